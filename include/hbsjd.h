@@ -1,0 +1,233 @@
+/*
+ * hbsjd.h - C ABI of the MI355X (gfx950) batched speculative-Jacobi rollout.
+ *
+ * The library replaces token-by-token student rollout in visual on-policy
+ * distillation (paper Sec. 3.1, Eq. 2: the student generates the suffix
+ * x_{k+1..T} after a real prefix x_{1..k}). Each image keeps its own committed
+ * cursor and window of W draft tokens (Sec. 4.2, "Independent rollout states");
+ * all images are verified together in one batched decoder forward over per-image
+ * positions and KV locations (Sec. 4.2, "Batched verification"); the
+ * probabilistic rule of Eq. 5 (accept with min(1, p/q), otherwise resample from
+ * [p - q]_+) or the greedy rule of Eq. 4 commits a variable number of tokens per
+ * image (Sec. 4.2, "Independent progress"); and each round runs either the full
+ * physical batch or only the active images, Full iff A > gamma (Sec. 4.3, Eq. 6).
+ *
+ * Conventions used by every call:
+ *  - Image tokens sit at sequence positions 1..T (T = grid^2); the class token
+ *    sits at position 0. Token arrays are row-major [batch][T]; entry t-1 of a
+ *    row is the token at position t.
+ *  - "device" pointers are HIP device memory of the GPU the context was created
+ *    on; "host" pointers are ordinary host memory. The caller owns every buffer
+ *    it passes in; the library never frees or keeps them after the call returns.
+ *  - Work is ordered on the context's stream. Calls that return results
+ *    (hbsjd_rollout, hbsjd_round, hbsjd_get_state, hbsjd_forward,
+ *    hbsjd_verify_probs, hbsjd_philox) block until those results are written.
+ *  - A context is used by one host thread at a time.
+ *  - Every call returns a status. On any status other than HBSJD_OK,
+ *    hbsjd_last_error() (per host thread) describes the failure. HBSJD_EINVAL
+ *    is returned before any device work is queued. HBSJD_EHIP and
+ *    HBSJD_EINTERNAL poison the context: later calls on it return HBSJD_ESTATE.
+ */
+#ifndef HBSJD_H_
+#define HBSJD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hbsjd_status {
+    HBSJD_OK = 0,
+    HBSJD_EINVAL = 1,     /* bad argument; nothing was queued */
+    HBSJD_ENOMEM = 2,     /* device allocation failed or exceeds the KV budget */
+    HBSJD_EHIP = 3,       /* a HIP runtime call failed */
+    HBSJD_ESTATE = 4,     /* call out of order, or the context is poisoned */
+    HBSJD_EINTERNAL = 5   /* a device-side invariant check failed */
+} hbsjd_status;
+
+typedef enum hbsjd_dtype {
+    HBSJD_DTYPE_F32 = 0,  /* fp32 weights, activations and KV cache */
+    HBSJD_DTYPE_BF16 = 1  /* bf16 weights and KV cache, fp32 accumulation and sampling */
+} hbsjd_dtype;
+
+typedef enum hbsjd_exec_mode {
+    HBSJD_EXEC_AUTO = 0,     /* per round: Full iff A > gamma (Sec. 4.3, Eq. 6) */
+    HBSJD_EXEC_FULL = 1,     /* every round processes all images, finished ones discarded */
+    HBSJD_EXEC_COMPACT = 2   /* every round processes only the active images */
+} hbsjd_exec_mode;
+
+typedef enum hbsjd_verify_mode {
+    HBSJD_VERIFY_PROB = 0,   /* Sec. 4.2, Eq. 5 */
+    HBSJD_VERIFY_GREEDY = 1  /* Sec. 4.2, Eq. 4 */
+} hbsjd_verify_mode;
+
+/*
+ * The student: a class-conditional LlamaGen-style decoder (Sec. 3.1, Eq. 1;
+ * the paper's students are LlamaGen-B and -L). Pre-norm blocks of RMSNorm ->
+ * QKV -> 2D RoPE -> causal attention -> O projection + residual -> RMSNorm ->
+ * SwiGLU MLP + residual; final RMSNorm and lm_head (optional bias).
+ * d_model must be a multiple of n_heads, head_dim = d_model / n_heads a
+ * multiple of 4; vocab a multiple of 4 and <= 16384. bf16 needs head_dim == 64
+ * and d_model, mlp_hidden and vocab multiples of 64; fp32 needs head_dim <= 64
+ * and grid^2 <= 959. Class index n_classes is the null class used by
+ * classifier-free guidance.
+ */
+typedef struct hbsjd_model_desc {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t mlp_hidden;
+    int32_t vocab;
+    int32_t n_classes;
+    int32_t grid;          /* image tokens T = grid * grid */
+    int32_t dtype;         /* hbsjd_dtype */
+    int32_t has_lm_bias;
+    float rms_eps;         /* e.g. 1e-5 */
+    float rope_base;       /* e.g. 10000 */
+} hbsjd_model_desc;
+
+typedef struct hbsjd_ctx hbsjd_ctx;
+
+/*
+ * Create a context on the current HIP device. `stream` is a hipStream_t (NULL
+ * for the default stream) on which all of the context's work is ordered.
+ * `max_kv_bytes` caps the KV-cache pool (0 = no cap). Returns EINVAL for an
+ * unsupported shape, ENOMEM, EHIP.
+ */
+hbsjd_status hbsjd_create(const hbsjd_model_desc* model, uint64_t max_kv_bytes, void* stream,
+                          hbsjd_ctx** out);
+
+/*
+ * Copy the weights to the device (rounding to bf16, nearest-even, for a bf16
+ * model). `host_blob` is fp32 host memory in this order, every matrix stored
+ * out x in row-major: tok_emb [V x d], cls_emb [(C+1) x d]; per layer g_attn [d],
+ * Wqkv [3d x d], Wo [d x d], g_ffn [d], W1 [f x d], W3 [f x d], W2 [d x f]; then
+ * g_out [d], W_lm [V x d] and, with has_lm_bias, b_lm [V]. EINVAL when
+ * n_floats does not match the model.
+ */
+hbsjd_status hbsjd_load_weights(hbsjd_ctx* ctx, const float* host_blob, size_t n_floats);
+
+/* Arguments of one rollout (the problem statement of Sec. 3.1, Eq. 2). */
+typedef struct hbsjd_rollout_args {
+    int32_t batch;                  /* B >= 1 */
+    const int32_t* prefix_tokens;   /* device [B][T]; the first prefix_len[b] entries are used */
+    const int32_t* prefix_len;      /* host [B]; k_b in [0, T]; image b generates T - k_b tokens */
+    const int32_t* class_labels;    /* host [B]; in [0, n_classes) */
+    const float* temperature;       /* host [B]; finite, > 0 */
+    int32_t window;                 /* W >= 1, Jacobi window (Sec. 4.2) */
+    int32_t history;                /* H >= 1, history offset of the draft fill (Sec. 4.2) */
+    int32_t top_k;                  /* 0 = off; otherwise keep entries >= the k-th largest */
+    float cfg_scale;                /* 0 = no guidance; else l_u + s (l_c - l_u) (Sec. 4.2) */
+    uint64_t seed;                  /* Philox key */
+    int32_t verify_mode;            /* hbsjd_verify_mode */
+    int32_t exec_mode;              /* hbsjd_exec_mode */
+    int32_t gamma;                  /* AUTO threshold; -1 = the context's calibrated value */
+    int32_t max_rounds;             /* capacity of `counts`; >= max_b (T - k_b) */
+} hbsjd_rollout_args;
+
+/* Results of one rollout; the caller allocates every array. */
+typedef struct hbsjd_rollout_out {
+    int32_t* tokens;            /* device [B][T]: the prefix, then the generated suffix */
+    int32_t* counts;            /* device [max_rounds][B]: tokens committed per round, 0 if inactive */
+    int32_t* rounds;            /* host [1]: verification rounds run */
+    int32_t* active_per_round;  /* host [max_rounds] or NULL: A at the start of each round */
+    int32_t* mode_per_round;    /* host [max_rounds] or NULL: 0 Full, 1 Compact */
+    int64_t* stats;             /* host [4] or NULL: drafts verified, drafts rejected,
+                                   image-rounds, verifier rows processed */
+} hbsjd_rollout_out;
+
+/*
+ * Run a whole rollout: prefill of [class, x_1..x_k] for every image, first
+ * draft from the student, then verification rounds until every image has T
+ * tokens. Blocking. The suffix of image b follows the student's AR distribution
+ * given its prefix (probabilistic mode) or the greedy AR sequence (greedy
+ * mode); Full, Compact and AUTO give identical results. EINVAL (before any
+ * device work) for B < 1, W < 1, H < 1, k_b outside [0, T], a label outside
+ * [0, C), a temperature that is not finite and positive, top_k < 0,
+ * max_rounds < max_b (T - k_b), or a prefix token outside [0, V) (found by a
+ * device check before the prefill). ENOMEM, EHIP, EINTERNAL.
+ */
+hbsjd_status hbsjd_rollout(hbsjd_ctx* ctx, const hbsjd_rollout_args* args,
+                           hbsjd_rollout_out* out);
+
+/* Round-level access for tests: prefill + first window (same checks as
+   hbsjd_rollout). The state lives in the context until the next begin. */
+hbsjd_status hbsjd_rollout_begin(hbsjd_ctx* ctx, const hbsjd_rollout_args* args);
+
+/*
+ * One verification round on the state made by hbsjd_rollout_begin, with an
+ * explicit execution mode (hbsjd_exec_mode; AUTO uses the begin call's gamma).
+ * `counts` host [B] receives the tokens committed this round (0 if inactive);
+ * `active` host [1] receives the number of images still active afterwards.
+ * ESTATE without a begin.
+ */
+hbsjd_status hbsjd_round(hbsjd_ctx* ctx, int32_t exec_mode, int32_t* counts, int32_t* active);
+
+/*
+ * Export the rollout state to host arrays (any may be NULL): tokens [B][T]
+ * (committed tokens, zero past the cursor), cursors [B] (committed count n_b),
+ * drafts [B][W] (window position n_b + 1 + j; -1 past T) and draft_reused [B][W]
+ * (1 if the draft is a reused prediction, 0 if a history token, -1 past T).
+ */
+hbsjd_status hbsjd_get_state(hbsjd_ctx* ctx, int32_t* tokens, int32_t* cursors, int32_t* drafts,
+                             int32_t* draft_reused);
+
+/*
+ * Teacher-forced forward of n_seqs sequences [class, x_1..x_len] through the
+ * same kernels (the prefill path). tokens: device [n_seqs][T]; lens, labels:
+ * host [n_seqs] (label n_classes = null class); logits: device fp32
+ * [sum_s (lens[s] + 1)][V], sequence after sequence, positions 0..len. Uses the
+ * rollout's KV pool (invalidates a rollout state).
+ */
+hbsjd_status hbsjd_forward(hbsjd_ctx* ctx, int32_t n_seqs, const int32_t* tokens,
+                           const int32_t* lens, const int32_t* labels, float* logits);
+
+/*
+ * The verification kernel (Sec. 4.2, Eq. 5) on caller-supplied rows, for
+ * testing. All pointers are device memory: p and q fp32 [B][W][V] (target and
+ * proposal row of draft j), drafts [B][W], u_acc [B][W], u_res [B]. Draft j is
+ * accepted iff p_j(z) >= q_j(z) or u_acc < p_j(z) / q_j(z); at the first
+ * rejection the replacement is drawn with u_res from [p_j - q_j]_+ (from p_j when
+ * that is all zero). Outputs: counts [B] (accepted drafts plus the replacement)
+ * and tokens [B][W] (-1 past the count). V <= 16384. Drafts must lie in
+ * [0, V); an image with a draft outside it gets count 0 and no tokens.
+ * `stream` may be NULL.
+ */
+hbsjd_status hbsjd_verify_probs(int32_t B, int32_t W, int32_t V, const float* p, const float* q,
+                                const int32_t* drafts, const float* u_acc, const float* u_res,
+                                int32_t* counts, int32_t* tokens, void* stream);
+
+/*
+ * Philox4x32-10 as the rollout uses it, for testing: key = seed, counter =
+ * (b, t, 0, 0) for each of the n pairs in `bt` (device uint32 [n][2]); writes
+ * device uint32 [n][4]. `stream` may be NULL.
+ */
+hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t* out,
+                          void* stream);
+
+/*
+ * Hardware calibration of the Full/Compact threshold (Sec. 4.3): times the
+ * verifier round at several active counts A <= batch in both modes on
+ * synthetic state and returns the largest A at which Compact is faster (the
+ * context keeps it for gamma = -1). Needs loaded weights; outputs do not
+ * depend on gamma.
+ */
+hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* ctx, int32_t batch, int32_t window,
+                                   int32_t* gamma);
+
+/* Release the context and its device memory (NULL is ignored). */
+void hbsjd_destroy(hbsjd_ctx* ctx);
+
+/* Description of the last failure on this host thread ("" if none). */
+const char* hbsjd_last_error(void);
+
+/* Library version string. */
+const char* hbsjd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HBSJD_H_ */

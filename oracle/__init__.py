@@ -25,7 +25,7 @@ def build(force: bool = False) -> str:
     """Compile the oracle with gcc: fp32, no contraction, no fast-math, OpenMP."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + f".tmp{os.getpid()}"
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
                                "-std=c11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
@@ -64,6 +64,7 @@ def lib():
             L.om_create.argtypes = [ctypes.POINTER(_Desc), _P, ctypes.c_long]
             L.om_free.argtypes = [_P]
             L.om_forward_seq.argtypes = [_P, ctypes.c_int, _P, ctypes.c_int, _P]
+            L.om_forward_batch.argtypes = [_P, ctypes.c_int] + [_P] * 6
             L.om_philox.argtypes = [ctypes.c_uint64, _P, _P]
             L.om_uniforms3.argtypes = [ctypes.c_uint64, ctypes.c_int, ctypes.c_int, _P]
             L.om_pinned_sum.restype = ctypes.c_float
@@ -133,6 +134,21 @@ class Model:
         if lib().om_forward_seq(self._h, int(cls), _ptr(tok), tok.size, _ptr(out)) != 0:
             raise ValueError("bad sequence length")
         return out
+
+    def forward_batch(self, classes, token_lists) -> list:
+        """forward_seq for several sequences, in parallel over sequences."""
+        n = len(token_lists)
+        lens = np.array([len(t) for t in token_lists], dtype=np.int32)
+        offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int32)
+        toks = np.ascontiguousarray(np.concatenate([np.asarray(t, dtype=np.int32).ravel()
+                                                    for t in token_lists] + [np.zeros(1, np.int32)]))
+        row0 = np.concatenate([[0], np.cumsum(lens + 1)[:-1]]).astype(np.int64)
+        cls = np.ascontiguousarray(classes, dtype=np.int32)
+        out = np.empty((int(np.sum(lens + 1)), self.shape.vocab), dtype=np.float32)
+        if lib().om_forward_batch(self._h, n, _ptr(cls), _ptr(toks), _ptr(offs), _ptr(lens),
+                                  _ptr(row0), _ptr(out)) != 0:
+            raise ValueError("bad sequence length")
+        return [out[row0[i]:row0[i] + lens[i] + 1] for i in range(n)]
 
     def rope(self, u: np.ndarray, pos: int) -> np.ndarray:
         v = np.ascontiguousarray(u, dtype=np.float32).copy()

@@ -329,6 +329,18 @@ int om_forward_seq(const om_model* o, int cls, const int* tok, int n, float* out
     return 0;
 }
 
+/* Teacher-forced forwards of n independent sequences (one per OpenMP task):
+   sequence s is [cls[s], tok[off[s]] .. tok[off[s] + len[s] - 1]], its logits go
+   to out rows row0[s] .. row0[s] + len[s]. */
+int om_forward_batch(const om_model* o, int n, const int* cls, const int* tok, const int* off,
+                     const int* len, const long* row0, float* out) {
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int s = 0; s < n; ++s)
+        bad |= om_forward_seq(o, cls[s], tok + off[s], len[s], out + row0[s] * o->m.V) != 0;
+    return bad ? -1 : 0;
+}
+
 /* ---------------------------------------------------------------- RNG */
 
 /* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the

@@ -1,0 +1,946 @@
+// C-ABI entry points and the host round driver of the batched SJD rollout.
+//
+// A rollout is: prefill of [class, x_1..x_k] for every image, first draft from
+// the student, then rounds of (active compaction + Full/Compact choice, row
+// assembly, decoder forward over the paged KV cache, lm_head, distribution
+// transform, verification, commit, window refresh) until every image holds T
+// tokens (paper Sec. 4.2-4.3). All of a round's launches read their row counts
+// from device memory written by the round's own set-up kernel, so the host
+// never waits inside a round; it reads the active count of the previous round
+// (pinned memory, one round behind) only to know when to stop. Rounds queued
+// after the last image finished process zero rows.
+#include "hbsjd.h"
+#include "common.h"
+#include "launch.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace hbsjd;
+
+namespace {
+
+thread_local std::string g_err;
+
+hbsjd_status fail(hbsjd_status st, const std::string& msg) {
+    g_err = msg;
+    return st;
+}
+
+struct DevBuf {
+    void* p = nullptr;
+    size_t n = 0;
+};
+
+}  // namespace
+
+struct hbsjd_ctx {
+    hbsjd_model_desc m{};
+    int L = 0, d = 0, H = 0, dh = 0, f = 0, V = 0, C = 0, G = 0, T = 0, nC = 0;
+    bool bf16 = false;
+    size_t esz = 4;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    uint64_t max_kv_bytes = 0;
+    bool poisoned = false;
+    bool weights = false;
+    int gamma_cal = -1;
+
+    // weights
+    DevBuf wbuf;
+    void *tok_emb = nullptr, *cls_emb = nullptr, *w_lm = nullptr;
+    float *b_lm = nullptr, *g_out = nullptr;
+    std::vector<float*> g_attn, g_ffn;
+    std::vector<void*> wqkv, wo, w13, w2;
+    DevBuf rope;   // cos then sin, [(T+1)][dh/2] each
+
+    // device buffers, grown on demand
+    DevBuf xtok, cursor, drafts, qsrc, labels, temps, plen;
+    DevBuf meta, meta_pf, a_hist, mode_hist, stats, counts_own;
+    DevBuf row_tok, row_pos, row_kv, row_seq;
+    DevBuf seg_seq, seg_row0, seg_nrows, seg_pos0;
+    DevBuf slot_img, active_list, pf_slots;
+    DevBuf h, hb, qb, ob, act;
+    DevBuf P[2], CP[2], amax[2], logits;
+    DevBuf seq_row0, seq_img, seq_branch, lm_idx;
+    DevBuf ptab, kv;
+    int32_t* pin = nullptr;    // pinned host words: active counts of the last two rounds
+    hipEvent_t ev[2] = {nullptr, nullptr};
+
+    // rollout state
+    bool have_state = false;
+    int B = 0, W = 0, Hh = 24, top_k = 0, cfg = 1, greedy = 0, exec_mode = 0, gamma = 0;
+    int max_rounds = 0, max_pages = 0, rounds_launched = 0;
+    float cfg_scale = 0.f;
+    uint64_t seed = 0;
+    int32_t* counts = nullptr;   // device [max_rounds][B]
+    long kv_layer_elems = 0;
+
+    ~hbsjd_ctx();
+};
+
+namespace {
+
+hbsjd_status hip_fail(hbsjd_ctx* c, hipError_t e, const char* what) {
+    if (c) c->poisoned = true;
+    return fail(HBSJD_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIPTRY(ctx, x)                                         \
+    do {                                                       \
+        hipError_t e_ = (x);                                   \
+        if (e_ != hipSuccess) return hip_fail((ctx), e_, #x);  \
+    } while (0)
+
+hbsjd_status ensure(hbsjd_ctx* c, DevBuf& b, size_t bytes) {
+    if (bytes == 0) bytes = 16;
+    if (b.n >= bytes) return HBSJD_OK;
+    if (b.p) {
+        HIPTRY(c, hipStreamSynchronize(c->stream));
+        HIPTRY(c, hipFree(b.p));
+        b.p = nullptr;
+        b.n = 0;
+    }
+    hipError_t e = hipMalloc(&b.p, bytes);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        b.p = nullptr;
+        return fail(HBSJD_ENOMEM, "device allocation of " + std::to_string(bytes) + " bytes failed");
+    }
+    b.n = bytes;
+    return HBSJD_OK;
+}
+
+#define TRY(x)                              \
+    do {                                    \
+        hbsjd_status s_ = (x);              \
+        if (s_ != HBSJD_OK) return s_;      \
+    } while (0)
+
+template <typename T> T* as(DevBuf& b) { return reinterpret_cast<T*>(b.p); }
+
+void free_buf(DevBuf& b) {
+    if (b.p) (void)hipFree(b.p);
+    b.p = nullptr;
+    b.n = 0;
+}
+
+}  // namespace
+
+hbsjd_ctx::~hbsjd_ctx() {
+    if (stream) (void)hipStreamSynchronize(stream);
+    DevBuf* all[] = {&wbuf, &rope, &xtok, &cursor, &drafts, &qsrc, &labels, &temps, &plen,
+                     &meta, &meta_pf, &a_hist, &mode_hist, &stats, &counts_own, &row_tok,
+                     &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
+                     &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &P[0], &P[1],
+                     &CP[0], &CP[1], &amax[0], &amax[1], &logits, &seq_row0, &seq_img,
+                     &seq_branch, &lm_idx, &ptab, &kv};
+    for (DevBuf* b : all) free_buf(*b);
+    if (pin) (void)hipHostFree(pin);
+    for (auto& e : ev)
+        if (e) (void)hipEventDestroy(e);
+}
+
+namespace {
+
+// ---------------------------------------------------------------- validation
+
+std::string check_model(const hbsjd_model_desc& m) {
+    if (m.n_layers < 1 || m.d_model < 4 || m.n_heads < 1 || m.mlp_hidden < 1 || m.vocab < 1 ||
+        m.n_classes < 1 || m.grid < 1)
+        return "model sizes must be positive";
+    if (m.d_model % m.n_heads) return "d_model must be a multiple of n_heads";
+    const int dh = m.d_model / m.n_heads;
+    if (dh % 4) return "head_dim must be a multiple of 4";
+    if (m.vocab > kMaxVocab) return "vocab must be <= 16384";
+    if (m.vocab % 4) return "vocab must be a multiple of 4";
+    if (m.dtype != HBSJD_DTYPE_F32 && m.dtype != HBSJD_DTYPE_BF16) return "unknown dtype";
+    if (m.dtype == HBSJD_DTYPE_BF16) {
+        if (dh != 64) return "bf16 needs head_dim 64";
+        if (m.d_model % 64) return "bf16 needs d_model a multiple of 64";
+        if (m.mlp_hidden % 64) return "bf16 needs mlp_hidden a multiple of 64";
+        if (m.vocab % 64) return "bf16 needs vocab a multiple of 64";
+    } else {
+        if (dh > 64) return "fp32 needs head_dim <= 64";
+        if ((long)m.grid * m.grid > 959) return "fp32 needs grid^2 <= 959";
+    }
+    if (!(m.rms_eps > 0.f) || !std::isfinite(m.rms_eps)) return "rms_eps must be positive";
+    if (!(m.rope_base > 0.f) || !std::isfinite(m.rope_base)) return "rope_base must be positive";
+    if ((long)m.grid * m.grid > 4096) return "grid too large";
+    return "";
+}
+
+size_t blob_floats(const hbsjd_ctx* c) {
+    const size_t d = c->d, f = c->f, V = c->V, C = c->C, L = c->L;
+    return V * d + (C + 1) * d + L * (2 * d + 3 * d * d + d * d + 3 * f * d) + d + V * d +
+           (c->m.has_lm_bias ? V : 0);
+}
+
+// ---------------------------------------------------------------- forward
+
+struct FwdRows {
+    RowMeta meta;
+    const int* nrows_dev;
+    int nrows_cap;
+    Segments seg;
+    const int* nseg_dev;
+    int nseg_cap;
+    int max_rows_per_seg;
+};
+
+void* kv_layer(hbsjd_ctx* c, int l) {
+    return (char*)c->kv.p + (size_t)l * c->kv_layer_elems * c->esz;
+}
+
+// decoder layers; leaves the residual stream in h (the final norm is the caller's)
+void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
+    const bool bf = c->bf16;
+    hipStream_t s = c->stream;
+    const int d = c->d, f = c->f;
+    embed_norm(bf, r.meta, r.nrows_dev, r.nrows_cap, c->tok_emb, c->cls_emb, c->g_attn[0],
+               c->m.rms_eps, d, as<float>(c->h), c->hb.p, s);
+    const float* rc = as<float>(c->rope);
+    const float* rs = rc + (size_t)(c->T + 1) * (c->dh / 2);
+    for (int l = 0; l < c->L; ++l) {
+        QkvArgs qa{c->qb.p, kv_layer(c, l), r.meta.pos, r.meta.kv, rc, rs, d, c->H, c->dh, c->T};
+        gemm_qkv(bf, c->hb.p, d, c->wqkv[l], 3 * d, d, r.nrows_dev, r.nrows_cap, qa, s);
+        attention(bf, c->qb.p, c->ob.p, d, c->H, c->dh, kv_layer(c, l), as<int32_t>(c->ptab),
+                  c->max_pages, r.seg, r.nseg_dev, r.nseg_cap, r.max_rows_per_seg, r.meta,
+                  r.nrows_dev, r.nrows_cap, s);
+        gemm_residual(bf, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap, as<float>(c->h), s);
+        rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_ffn[l], c->m.rms_eps,
+                d, c->hb.p, s);
+        gemm_swiglu(bf, c->hb.p, d, c->w13[l], 2 * f, d, r.nrows_dev, r.nrows_cap, c->act.p, s);
+        gemm_residual(bf, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap, as<float>(c->h), s);
+        if (l + 1 < c->L)
+            rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_attn[l + 1],
+                    c->m.rms_eps, d, c->hb.p, s);
+    }
+}
+
+// activation buffers for `rows` rows
+hbsjd_status ensure_acts(hbsjd_ctx* c, long rows) {
+    const size_t d = c->d, f = c->f;
+    TRY(ensure(c, c->h, rows * d * 4));
+    TRY(ensure(c, c->hb, rows * d * c->esz));
+    TRY(ensure(c, c->qb, rows * d * c->esz));
+    TRY(ensure(c, c->ob, rows * d * c->esz));
+    TRY(ensure(c, c->act, rows * f * c->esz));
+    TRY(ensure(c, c->row_tok, rows * 4));
+    TRY(ensure(c, c->row_pos, rows * 4));
+    TRY(ensure(c, c->row_kv, rows * 4));
+    TRY(ensure(c, c->row_seq, rows * 4));
+    return HBSJD_OK;
+}
+
+// page table and KV pool for n_seq sequences of cap positions each
+hbsjd_status ensure_kv(hbsjd_ctx* c, int n_seq, int cap) {
+    c->max_pages = (cap + kPage - 1) / kPage;
+    const long pages = (long)n_seq * c->max_pages;
+    const long page_elems = 2L * kPage * c->d;
+    c->kv_layer_elems = pages * page_elems;
+    const size_t bytes = (size_t)c->L * c->kv_layer_elems * c->esz;
+    if (c->max_kv_bytes && bytes > c->max_kv_bytes)
+        return fail(HBSJD_ENOMEM, "KV cache needs " + std::to_string(bytes) +
+                                      " bytes, above the context's cap");
+    const bool grow = c->kv.n < bytes;
+    TRY(ensure(c, c->kv, bytes));
+    if (grow) HIPTRY(c, hipMemsetAsync(c->kv.p, 0, c->kv.n, c->stream));
+    // page of (sequence q, tile j) = j * n_seq + q: pages of one sequence are not adjacent
+    std::vector<int32_t> pt((size_t)n_seq * c->max_pages);
+    for (int q = 0; q < n_seq; ++q)
+        for (int j = 0; j < c->max_pages; ++j) pt[(size_t)q * c->max_pages + j] = j * n_seq + q;
+    TRY(ensure(c, c->ptab, pt.size() * 4));
+    HIPTRY(c, hipMemcpyAsync(c->ptab.p, pt.data(), pt.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIPTRY(c, hipStreamSynchronize(c->stream));
+    return HBSJD_OK;
+}
+
+hbsjd_status check_device_error(hbsjd_ctx* c) {
+    int32_t err = 0;
+    HIPTRY(c, hipMemcpyAsync(&err, as<int32_t>(c->meta) + kMetaError, 4, hipMemcpyDeviceToHost,
+                             c->stream));
+    HIPTRY(c, hipStreamSynchronize(c->stream));
+    if (err) {
+        c->poisoned = true;
+        std::string why;
+        if (err & kErrNanLogit) why += " NaN logit;";
+        if (err & kErrZeroProposal) why += " zero proposal probability of a reused draft;";
+        if (err & kErrBadToken) why += " token out of range;";
+        if (err & kErrRoundOverflow) why += " more rounds than max_rounds;";
+        return fail(HBSJD_EINTERNAL, "device check failed:" + why);
+    }
+    return HBSJD_OK;
+}
+
+// ---------------------------------------------------------------- rollout set-up
+
+hbsjd_status validate_args(const hbsjd_ctx* c, const hbsjd_rollout_args* a) {
+    if (!a) return fail(HBSJD_EINVAL, "args is NULL");
+    if (a->batch < 1) return fail(HBSJD_EINVAL, "batch must be >= 1");
+    if (a->window < 1 || a->window > 64) return fail(HBSJD_EINVAL, "window must be in [1, 64]");
+    if (a->history < 1) return fail(HBSJD_EINVAL, "history must be >= 1");
+    if (a->top_k < 0) return fail(HBSJD_EINVAL, "top_k must be >= 0");
+    if (!std::isfinite(a->cfg_scale)) return fail(HBSJD_EINVAL, "cfg_scale must be finite");
+    if (a->verify_mode != HBSJD_VERIFY_PROB && a->verify_mode != HBSJD_VERIFY_GREEDY)
+        return fail(HBSJD_EINVAL, "unknown verify_mode");
+    if (a->exec_mode < HBSJD_EXEC_AUTO || a->exec_mode > HBSJD_EXEC_COMPACT)
+        return fail(HBSJD_EINVAL, "unknown exec_mode");
+    if (a->gamma < -1) return fail(HBSJD_EINVAL, "gamma must be >= -1");
+    if (!a->prefix_tokens || !a->prefix_len || !a->class_labels || !a->temperature)
+        return fail(HBSJD_EINVAL, "prefix_tokens, prefix_len, class_labels and temperature are required");
+    if (!c->bf16 && c->T + a->window + 1 > 1024)
+        return fail(HBSJD_EINVAL, "fp32 mode supports T + window + 1 <= 1024");
+    int need = 0;
+    for (int b = 0; b < a->batch; ++b) {
+        const int k = a->prefix_len[b];
+        if (k < 0 || k > c->T) return fail(HBSJD_EINVAL, "prefix_len out of [0, T]");
+        if (a->class_labels[b] < 0 || a->class_labels[b] >= c->C)
+            return fail(HBSJD_EINVAL, "class label out of [0, n_classes)");
+        const float tau = a->temperature[b];
+        if (!std::isfinite(tau) || !(tau > 0.f))
+            return fail(HBSJD_EINVAL, "temperature must be finite and > 0");
+        need = std::max(need, c->T - k);
+    }
+    if (a->max_rounds < need) return fail(HBSJD_EINVAL, "max_rounds below max_b (T - k_b)");
+    return HBSJD_OK;
+}
+
+hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_dev) {
+    if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
+    TRY(validate_args(c, a));
+    hipStream_t s = c->stream;
+    const int B = a->batch, T = c->T, W = a->window;
+    c->have_state = false;
+    c->B = B;
+    c->W = W;
+    c->Hh = a->history;
+    c->top_k = a->top_k;
+    c->cfg = a->cfg_scale != 0.f ? 2 : 1;
+    c->cfg_scale = a->cfg_scale;
+    c->greedy = a->verify_mode == HBSJD_VERIFY_GREEDY;
+    c->exec_mode = a->exec_mode;
+    c->gamma = a->gamma >= 0 ? a->gamma : (c->gamma_cal >= 0 ? c->gamma_cal : B / 2);
+    c->seed = a->seed;
+    c->max_rounds = a->max_rounds;
+    c->rounds_launched = 0;
+    const int cfg = c->cfg;
+    const int S = B * cfg;
+
+    // prefill geometry (host knows the lengths)
+    std::vector<int32_t> row0(1, 0), simg, sbr, lidx, pslots;
+    int maxlen = 0;
+    for (int b = 0; b < B; ++b) {
+        const int k = a->prefix_len[b];
+        if (k >= T) continue;
+        pslots.push_back(b);
+        for (int br = 0; br < cfg; ++br) {
+            simg.push_back(b);
+            sbr.push_back(br);
+            lidx.push_back(row0.back() + k);
+            row0.push_back(row0.back() + k + 1);
+        }
+        maxlen = std::max(maxlen, k + 1);
+    }
+    const int n_seq = (int)simg.size();
+    const int pf_rows = row0.back();
+    const long round_rows = (long)S * (W + 1);
+    const long out_rows = (long)B * (W + 1);
+
+    TRY(ensure_acts(c, std::max<long>(pf_rows, round_rows)));
+    TRY(ensure_kv(c, S, T + W + 1));
+    TRY(ensure(c, c->xtok, (size_t)B * T * 4));
+    TRY(ensure(c, c->cursor, B * 4));
+    TRY(ensure(c, c->drafts, (size_t)B * W * 4));
+    TRY(ensure(c, c->qsrc, (size_t)B * W * 4));
+    TRY(ensure(c, c->labels, B * 4));
+    TRY(ensure(c, c->temps, B * 4));
+    TRY(ensure(c, c->plen, B * 4));
+    TRY(ensure(c, c->meta, kMetaCount * 4));
+    TRY(ensure(c, c->meta_pf, kMetaCount * 4));
+    TRY(ensure(c, c->a_hist, (size_t)(a->max_rounds + 1) * 4));
+    TRY(ensure(c, c->mode_hist, (size_t)(a->max_rounds + 1) * 4));
+    TRY(ensure(c, c->stats, 4 * 8));
+    TRY(ensure(c, c->seg_seq, S * 4));
+    TRY(ensure(c, c->seg_row0, std::max(S, n_seq + 1) * 4));
+    TRY(ensure(c, c->seg_nrows, S * 4));
+    TRY(ensure(c, c->seg_pos0, S * 4));
+    TRY(ensure(c, c->slot_img, B * 4));
+    TRY(ensure(c, c->active_list, B * 4));
+    TRY(ensure(c, c->pf_slots, B * 4));
+    TRY(ensure(c, c->seq_row0, (n_seq + 1) * 4));
+    TRY(ensure(c, c->seq_img, std::max(n_seq, 1) * 4));
+    TRY(ensure(c, c->seq_branch, std::max(n_seq, 1) * 4));
+    TRY(ensure(c, c->lm_idx, std::max(n_seq, 1) * 4));
+    for (int k = 0; k < 2; ++k) {
+        TRY(ensure(c, c->P[k], (size_t)(cfg == 1 ? round_rows : out_rows) * c->V * 4));
+        TRY(ensure(c, c->CP[k], (size_t)out_rows * (c->nC + 1) * 4));
+        TRY(ensure(c, c->amax[k], (size_t)out_rows * 4));
+    }
+    if (cfg == 2) TRY(ensure(c, c->logits, (size_t)round_rows * c->V * 4));
+    if (!counts_dev) {
+        TRY(ensure(c, c->counts_own, (size_t)a->max_rounds * B * 4));
+        counts_dev = as<int32_t>(c->counts_own);
+    }
+    c->counts = counts_dev;
+    if (!c->pin) {
+        HIPTRY(c, hipHostMalloc((void**)&c->pin, 64, hipHostMallocDefault));
+        HIPTRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
+        HIPTRY(c, hipEventCreateWithFlags(&c->ev[1], hipEventDisableTiming));
+    }
+
+    // state
+    std::vector<int32_t> meta(kMetaCount, 0);
+    meta[kMetaRound] = -1;
+    HIPTRY(c, hipMemcpyAsync(c->meta.p, meta.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->xtok.p, a->prefix_tokens, (size_t)B * T * 4, hipMemcpyDeviceToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->cursor.p, a->prefix_len, B * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->plen.p, a->prefix_len, B * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->labels.p, a->class_labels, B * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->temps.p, a->temperature, B * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemsetAsync(c->drafts.p, 0xff, (size_t)B * W * 4, s));
+    HIPTRY(c, hipMemsetAsync(c->qsrc.p, 0xff, (size_t)B * W * 4, s));
+    HIPTRY(c, hipMemsetAsync(c->stats.p, 0, 32, s));
+    HIPTRY(c, hipMemsetAsync(c->counts, 0, (size_t)a->max_rounds * B * 4, s));
+    check_prefix(as<int32_t>(c->xtok), as<int32_t>(c->plen), B, T, c->V,
+                 as<int32_t>(c->meta) + kMetaError, s);
+    {
+        int32_t err = 0;
+        HIPTRY(c, hipMemcpyAsync(&err, as<int32_t>(c->meta) + kMetaError, 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipStreamSynchronize(s));
+        if (err) return fail(HBSJD_EINVAL, "a prefix token is outside [0, vocab)");
+    }
+    if (n_seq == 0) {
+        c->have_state = true;
+        return HBSJD_OK;
+    }
+
+    // prefill rows and segments
+    std::vector<int32_t> segseq(n_seq), segrow0(n_seq), segn(n_seq), segpos(n_seq, 0);
+    for (int q = 0; q < n_seq; ++q) {
+        segseq[q] = simg[q] * cfg + sbr[q];
+        segrow0[q] = row0[q];
+        segn[q] = row0[q + 1] - row0[q];
+    }
+    HIPTRY(c, hipMemcpyAsync(c->seq_row0.p, row0.data(), (n_seq + 1) * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seq_img.p, simg.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seq_branch.p, sbr.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->lm_idx.p, lidx.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->pf_slots.p, pslots.data(), pslots.size() * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_seq.p, segseq.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, segrow0.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    std::vector<int32_t> mpf(kMetaCount, 0);
+    mpf[kMetaRows] = pf_rows;
+    mpf[kMetaSegs] = n_seq;
+    mpf[kMetaOutRows] = (int)pslots.size();
+    mpf[kMetaImgs] = (int)pslots.size();
+    mpf[kMetaActive] = n_seq;     // rows of the lm_head
+    HIPTRY(c, hipMemcpyAsync(c->meta_pf.p, mpf.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+    // the host staging vectors must outlive the async copies
+    HIPTRY(c, hipStreamSynchronize(s));
+
+    PrefillRowsArgs pa{n_seq, T, cfg, c->C, c->max_pages, pf_rows, as<int32_t>(c->seq_row0),
+                       as<int32_t>(c->seq_img), as<int32_t>(c->seq_branch), as<int32_t>(c->xtok),
+                       as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->row_tok),
+                       as<int32_t>(c->row_pos), as<int32_t>(c->row_kv), as<int32_t>(c->row_seq)};
+    prefill_rows(pa, s);
+    int32_t* mp = as<int32_t>(c->meta_pf);
+    FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
+                       as<int32_t>(c->row_seq)},
+               mp + kMetaRows, pf_rows,
+               Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows),
+                        as<int32_t>(c->seg_pos0)},
+               mp + kMetaSegs, n_seq, maxlen};
+    forward_layers(c, fr);
+    // final norm of each sequence's last row, lm_head, transform, first window
+    rmsnorm(c->bf16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, n_seq, c->g_out,
+            c->m.rms_eps, c->d, c->hb.p, s);
+    float* lg = cfg == 1 ? as<float>(c->P[1]) : as<float>(c->logits);
+    gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, n_seq, lg, c->b_lm, s);
+    TransformArgs ta{lg, as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
+                     as<int32_t>(c->pf_slots), as<float>(c->temps), 1, cfg, c->V, c->top_k,
+                     c->cfg_scale, mp + kMetaOutRows, (int)pslots.size(), as<int32_t>(c->meta)};
+    transform(ta, s);
+    VerifyArgs va{B, W, T, c->Hh, c->V, c->greedy, 1, 1, c->max_rounds, c->seed,
+                  as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]), nullptr,
+                  as<int32_t>(c->pf_slots), mp + kMetaImgs, (int)pslots.size(),
+                  as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
+                  as<int32_t>(c->qsrc), nullptr, as<int64_t>(c->stats), as<int32_t>(c->meta)};
+    verify_commit(va, s);
+    HIPTRY(c, hipGetLastError());
+    c->have_state = true;
+    return HBSJD_OK;
+}
+
+// queue one round (parity r & 1); every launch sizes itself from device counts
+hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
+    hipStream_t s = c->stream;
+    const int r = c->rounds_launched;
+    const int cur = r & 1;
+    const int B = c->B, W = c->W, cfg = c->cfg, S = B * cfg, R = W + 1;
+    int32_t* mt = as<int32_t>(c->meta);
+    RoundSetupArgs sa{B, W, c->T, cfg, c->C, c->gamma, exec_mode, c->max_pages, c->max_rounds,
+                      as<int32_t>(c->cursor), as<int32_t>(c->drafts), as<int32_t>(c->xtok),
+                      as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->slot_img),
+                      as<int32_t>(c->active_list), as<int32_t>(c->row_tok), as<int32_t>(c->row_pos),
+                      as<int32_t>(c->row_kv), as<int32_t>(c->row_seq), as<int32_t>(c->seg_seq),
+                      as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0),
+                      mt, as<int32_t>(c->a_hist), as<int32_t>(c->mode_hist)};
+    round_setup(sa, s);
+    const int rows_cap = S * R;
+    FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
+                       as<int32_t>(c->row_seq)},
+               mt + kMetaRows, rows_cap,
+               Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows),
+                        as<int32_t>(c->seg_pos0)},
+               mt + kMetaSegs, S, R};
+    forward_layers(c, fr);
+    rmsnorm(c->bf16, as<float>(c->h), nullptr, mt + kMetaRows, rows_cap, c->g_out, c->m.rms_eps,
+            c->d, c->hb.p, s);
+    float* lg = cfg == 1 ? as<float>(c->P[cur]) : as<float>(c->logits);
+    gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg, c->b_lm, s);
+    TransformArgs ta{lg, as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
+                     as<int32_t>(c->slot_img), as<float>(c->temps), R, cfg, c->V, c->top_k,
+                     c->cfg_scale, mt + kMetaOutRows, B * R, mt};
+    transform(ta, s);
+    VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds, c->seed,
+                  as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
+                  as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
+                  as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
+                  as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt};
+    verify_commit(va, s);
+    HIPTRY(c, hipGetLastError());
+    c->rounds_launched = r + 1;
+    return HBSJD_OK;
+}
+
+#define GUARD(ctx)                                                                       \
+    if (!(ctx)) return fail(HBSJD_EINVAL, "ctx is NULL");                                \
+    if ((ctx)->poisoned) return fail(HBSJD_ESTATE, "context is poisoned by an earlier failure"); \
+    HIPTRY(ctx, hipSetDevice((ctx)->device))
+
+}  // namespace
+
+// ==================================================================== C ABI
+
+extern "C" {
+
+const char* hbsjd_last_error(void) { return g_err.c_str(); }
+
+const char* hbsjd_version(void) { return "hbsjd-gfx950 0.1"; }
+
+hbsjd_status hbsjd_create(const hbsjd_model_desc* m, uint64_t max_kv_bytes, void* stream,
+                          hbsjd_ctx** out) {
+    try {
+        if (!m || !out) return fail(HBSJD_EINVAL, "model and out must not be NULL");
+        *out = nullptr;
+        const std::string why = check_model(*m);
+        if (!why.empty()) return fail(HBSJD_EINVAL, why);
+        hbsjd_ctx* c = new hbsjd_ctx();
+        c->m = *m;
+        c->L = m->n_layers;
+        c->d = m->d_model;
+        c->H = m->n_heads;
+        c->dh = m->d_model / m->n_heads;
+        c->f = m->mlp_hidden;
+        c->V = m->vocab;
+        c->C = m->n_classes;
+        c->G = m->grid;
+        c->T = m->grid * m->grid;
+        c->nC = (c->V + kChunk - 1) / kChunk;
+        c->bf16 = m->dtype == HBSJD_DTYPE_BF16;
+        c->esz = c->bf16 ? 2 : 4;
+        c->stream = (hipStream_t)stream;
+        c->max_kv_bytes = max_kv_bytes;
+        hipError_t e = hipGetDevice(&c->device);
+        if (e != hipSuccess) {
+            delete c;
+            return fail(HBSJD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+        }
+        // 2D RoPE tables: position s >= 1 is grid cell (row, col) = divmod(s - 1, G);
+        // pair i < dh/4 turns by row * base^(-4i/dh), pair i >= dh/4 by
+        // col * base^(-4(i - dh/4)/dh); position 0 (class token) is not turned.
+        const int half = c->dh / 2, quarter = c->dh / 4;
+        std::vector<float> tab((size_t)2 * (c->T + 1) * half);
+        float* cs = tab.data();
+        float* sn = tab.data() + (size_t)(c->T + 1) * half;
+        for (int s = 0; s <= c->T; ++s) {
+            const int row = s ? (s - 1) / c->G : 0, col = s ? (s - 1) % c->G : 0;
+            for (int i = 0; i < half; ++i) {
+                const int ii = i < quarter ? i : i - quarter;
+                const double theta = std::pow((double)m->rope_base, -4.0 * ii / (double)c->dh);
+                const double ang = s ? (i < quarter ? row : col) * theta : 0.0;
+                cs[(size_t)s * half + i] = (float)std::cos(ang);
+                sn[(size_t)s * half + i] = (float)std::sin(ang);
+            }
+        }
+        hbsjd_status st = ensure(c, c->rope, tab.size() * 4);
+        if (st != HBSJD_OK) {
+            delete c;
+            return st;
+        }
+        e = hipMemcpy(c->rope.p, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            delete c;
+            return fail(HBSJD_EHIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+        }
+        *out = c;
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_create");
+    }
+}
+
+void hbsjd_destroy(hbsjd_ctx* ctx) {
+    if (!ctx) return;
+    (void)hipSetDevice(ctx->device);
+    delete ctx;
+}
+
+hbsjd_status hbsjd_load_weights(hbsjd_ctx* c, const float* blob, size_t n_floats) {
+    try {
+        GUARD(c);
+        if (!blob) return fail(HBSJD_EINVAL, "blob is NULL");
+        if (n_floats != blob_floats(c))
+            return fail(HBSJD_EINVAL, "blob has " + std::to_string(n_floats) + " floats, model needs " +
+                                          std::to_string(blob_floats(c)));
+        const size_t d = c->d, f = c->f, V = c->V, C = c->C, L = c->L, es = c->esz;
+        // device layout: matrices in the compute dtype, gains and bias fp32,
+        // W1|W3 interleaved by rows (row 2i = W1 row i, row 2i+1 = W3 row i)
+        std::vector<size_t> off;
+        size_t total = 0;
+        auto take = [&](size_t bytes) {
+            off.push_back(total);
+            total += (bytes + 255) & ~(size_t)255;
+        };
+        take(V * d * es);            // tok_emb
+        take((C + 1) * d * es);      // cls_emb
+        for (size_t l = 0; l < L; ++l) {
+            take(d * 4);             // g_attn
+            take(3 * d * d * es);    // wqkv
+            take(d * d * es);        // wo
+            take(d * 4);             // g_ffn
+            take(2 * f * d * es);    // w13
+            take(d * f * es);        // w2
+        }
+        take(d * 4);                 // g_out
+        take(V * d * es);            // w_lm
+        if (c->m.has_lm_bias) take(V * 4);
+        std::vector<unsigned char> host(total, 0);
+        auto put = [&](size_t dst, const float* src, size_t n, bool mat) {
+            if (mat && c->bf16) {
+                uint16_t* o = reinterpret_cast<uint16_t*>(host.data() + dst);
+                for (size_t i = 0; i < n; ++i) o[i] = f32_to_bf16(src[i]);
+            } else {
+                std::memcpy(host.data() + dst, src, n * 4);
+            }
+        };
+        const float* p = blob;
+        size_t k = 0;
+        put(off[k++], p, V * d, true); p += V * d;
+        put(off[k++], p, (C + 1) * d, true); p += (C + 1) * d;
+        for (size_t l = 0; l < L; ++l) {
+            put(off[k++], p, d, false); p += d;
+            put(off[k++], p, 3 * d * d, true); p += 3 * d * d;
+            put(off[k++], p, d * d, true); p += d * d;
+            put(off[k++], p, d, false); p += d;
+            {
+                const float* w1 = p;
+                const float* w3 = p + f * d;
+                std::vector<float> il(2 * f * d);
+                for (size_t i = 0; i < f; ++i) {
+                    std::memcpy(&il[(2 * i) * d], w1 + i * d, d * 4);
+                    std::memcpy(&il[(2 * i + 1) * d], w3 + i * d, d * 4);
+                }
+                put(off[k++], il.data(), 2 * f * d, true);
+                p += 2 * f * d;
+            }
+            put(off[k++], p, d * f, true); p += d * f;
+        }
+        put(off[k++], p, d, false); p += d;
+        put(off[k++], p, V * d, true); p += V * d;
+        if (c->m.has_lm_bias) { put(off[k++], p, V, false); p += V; }
+        TRY(ensure(c, c->wbuf, total));
+        HIPTRY(c, hipMemcpy(c->wbuf.p, host.data(), total, hipMemcpyHostToDevice));
+        char* base = (char*)c->wbuf.p;
+        k = 0;
+        c->tok_emb = base + off[k++];
+        c->cls_emb = base + off[k++];
+        c->g_attn.assign(L, nullptr); c->g_ffn.assign(L, nullptr);
+        c->wqkv.assign(L, nullptr); c->wo.assign(L, nullptr);
+        c->w13.assign(L, nullptr); c->w2.assign(L, nullptr);
+        for (size_t l = 0; l < L; ++l) {
+            c->g_attn[l] = (float*)(base + off[k++]);
+            c->wqkv[l] = base + off[k++];
+            c->wo[l] = base + off[k++];
+            c->g_ffn[l] = (float*)(base + off[k++]);
+            c->w13[l] = base + off[k++];
+            c->w2[l] = base + off[k++];
+        }
+        c->g_out = (float*)(base + off[k++]);
+        c->w_lm = base + off[k++];
+        c->b_lm = c->m.has_lm_bias ? (float*)(base + off[k++]) : nullptr;
+        c->weights = true;
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_load_weights");
+    }
+}
+
+hbsjd_status hbsjd_rollout_begin(hbsjd_ctx* c, const hbsjd_rollout_args* a) {
+    try {
+        GUARD(c);
+        TRY(begin(c, a, nullptr));
+        HIPTRY(c, hipStreamSynchronize(c->stream));
+        return check_device_error(c);
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_rollout_begin");
+    }
+}
+
+hbsjd_status hbsjd_rollout(hbsjd_ctx* c, const hbsjd_rollout_args* a, hbsjd_rollout_out* o) {
+    try {
+        GUARD(c);
+        if (!o || !o->tokens || !o->counts || !o->rounds)
+            return fail(HBSJD_EINVAL, "out.tokens, out.counts and out.rounds are required");
+        TRY(begin(c, a, o->counts));
+        hipStream_t s = c->stream;
+        int rounds = 0;
+        // the host stays one round behind the device: it reads A of round r-1
+        // while round r is queued; A = 0 means round r-1 (and r) had no work
+        for (int r = 0;; ++r) {
+            if (r > c->max_rounds + 2) {
+                c->poisoned = true;
+                return fail(HBSJD_EINTERNAL, "round watchdog: rollout did not finish");
+            }
+            TRY(launch_round(c, c->exec_mode));
+            HIPTRY(c, hipMemcpyAsync(c->pin + (r & 1), as<int32_t>(c->meta) + kMetaActive, 4,
+                                     hipMemcpyDeviceToHost, s));
+            HIPTRY(c, hipEventRecord(c->ev[r & 1], s));
+            if (r >= 1) {
+                HIPTRY(c, hipEventSynchronize(c->ev[(r - 1) & 1]));
+                if (c->pin[(r - 1) & 1] == 0) {
+                    rounds = r - 1;
+                    break;
+                }
+            }
+        }
+        HIPTRY(c, hipMemcpyAsync(o->tokens, c->xtok.p, (size_t)c->B * c->T * 4,
+                                 hipMemcpyDeviceToDevice, s));
+        std::vector<int32_t> ah(rounds + 1), mh(rounds + 1);
+        int64_t st[4] = {0, 0, 0, 0};
+        if (rounds > 0) {
+            HIPTRY(c, hipMemcpyAsync(ah.data(), c->a_hist.p, rounds * 4, hipMemcpyDeviceToHost, s));
+            HIPTRY(c, hipMemcpyAsync(mh.data(), c->mode_hist.p, rounds * 4, hipMemcpyDeviceToHost, s));
+        }
+        HIPTRY(c, hipMemcpyAsync(st, c->stats.p, 32, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipStreamSynchronize(s));
+        TRY(check_device_error(c));
+        *o->rounds = rounds;
+        int64_t rows = 0;
+        for (int r = 0; r < rounds; ++r) {
+            const int nimg = ah[r] == 0 ? 0 : (mh[r] == 0 ? c->B : ah[r]);
+            rows += (int64_t)nimg * c->cfg * (c->W + 1);
+        }
+        if (o->active_per_round) std::memcpy(o->active_per_round, ah.data(), rounds * 4);
+        if (o->mode_per_round) std::memcpy(o->mode_per_round, mh.data(), rounds * 4);
+        if (o->stats) {
+            o->stats[0] = st[0];
+            o->stats[1] = st[1];
+            o->stats[2] = st[2];
+            o->stats[3] = rows;
+        }
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_rollout");
+    }
+}
+
+hbsjd_status hbsjd_round(hbsjd_ctx* c, int32_t exec_mode, int32_t* counts, int32_t* active) {
+    try {
+        GUARD(c);
+        if (!c->have_state) return fail(HBSJD_ESTATE, "no rollout state: call hbsjd_rollout_begin");
+        if (exec_mode < HBSJD_EXEC_AUTO || exec_mode > HBSJD_EXEC_COMPACT)
+            return fail(HBSJD_EINVAL, "unknown exec_mode");
+        if (c->rounds_launched >= c->max_rounds) return fail(HBSJD_ESTATE, "max_rounds reached");
+        const int r = c->rounds_launched;
+        TRY(launch_round(c, exec_mode));
+        std::vector<int32_t> cur(c->B);
+        if (counts)
+            HIPTRY(c, hipMemcpyAsync(counts, c->counts + (size_t)r * c->B, c->B * 4,
+                                     hipMemcpyDeviceToHost, c->stream));
+        HIPTRY(c, hipMemcpyAsync(cur.data(), c->cursor.p, c->B * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPTRY(c, hipStreamSynchronize(c->stream));
+        TRY(check_device_error(c));
+        if (active) {
+            int n = 0;
+            for (int b = 0; b < c->B; ++b) n += cur[b] < c->T;
+            *active = n;
+        }
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_round");
+    }
+}
+
+hbsjd_status hbsjd_get_state(hbsjd_ctx* c, int32_t* tokens, int32_t* cursors, int32_t* drafts,
+                             int32_t* draft_reused) {
+    try {
+        GUARD(c);
+        if (!c->have_state) return fail(HBSJD_ESTATE, "no rollout state");
+        const int B = c->B, T = c->T, W = c->W;
+        std::vector<int32_t> x((size_t)B * T), n(B), dr((size_t)B * W), qs((size_t)B * W);
+        hipStream_t s = c->stream;
+        HIPTRY(c, hipMemcpyAsync(x.data(), c->xtok.p, x.size() * 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipMemcpyAsync(n.data(), c->cursor.p, B * 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipMemcpyAsync(dr.data(), c->drafts.p, dr.size() * 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipMemcpyAsync(qs.data(), c->qsrc.p, qs.size() * 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipStreamSynchronize(s));
+        for (int b = 0; b < B; ++b)
+            for (int t = n[b]; t < T; ++t) x[(size_t)b * T + t] = 0;
+        if (tokens) std::memcpy(tokens, x.data(), x.size() * 4);
+        if (cursors) std::memcpy(cursors, n.data(), B * 4);
+        if (drafts) std::memcpy(drafts, dr.data(), dr.size() * 4);
+        if (draft_reused)
+            for (size_t i = 0; i < qs.size(); ++i) draft_reused[i] = dr[i] < 0 ? -1 : (qs[i] >= 0 ? 1 : 0);
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_get_state");
+    }
+}
+
+hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
+                           const int32_t* lens, const int32_t* labels, float* logits) {
+    try {
+        GUARD(c);
+        if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
+        if (n_seqs < 1 || !tokens || !lens || !labels || !logits)
+            return fail(HBSJD_EINVAL, "bad forward arguments");
+        std::vector<int32_t> row0(1, 0), simg, sbr, pl(n_seqs), lab(n_seqs);
+        int maxlen = 0;
+        for (int q = 0; q < n_seqs; ++q) {
+            if (lens[q] < 0 || lens[q] > c->T) return fail(HBSJD_EINVAL, "length out of [0, T]");
+            if (labels[q] < 0 || labels[q] > c->C) return fail(HBSJD_EINVAL, "label out of [0, n_classes]");
+            simg.push_back(q);
+            sbr.push_back(0);
+            row0.push_back(row0.back() + lens[q] + 1);
+            maxlen = std::max(maxlen, lens[q] + 1);
+            pl[q] = lens[q];
+            lab[q] = labels[q];
+        }
+        hipStream_t s = c->stream;
+        const int rows = row0.back();
+        c->have_state = false;
+        TRY(ensure_acts(c, rows));
+        TRY(ensure_kv(c, n_seqs, c->T + 1));
+        TRY(ensure(c, c->meta, kMetaCount * 4));
+        TRY(ensure(c, c->meta_pf, kMetaCount * 4));
+        TRY(ensure(c, c->plen, n_seqs * 4));
+        TRY(ensure(c, c->labels, n_seqs * 4));
+        TRY(ensure(c, c->seq_row0, (n_seqs + 1) * 4));
+        TRY(ensure(c, c->seq_img, n_seqs * 4));
+        TRY(ensure(c, c->seq_branch, n_seqs * 4));
+        TRY(ensure(c, c->seg_seq, n_seqs * 4));
+        TRY(ensure(c, c->seg_row0, (n_seqs + 1) * 4));
+        TRY(ensure(c, c->seg_nrows, n_seqs * 4));
+        TRY(ensure(c, c->seg_pos0, n_seqs * 4));
+        std::vector<int32_t> segn(n_seqs), segpos(n_seqs, 0), mz(kMetaCount, 0);
+        for (int q = 0; q < n_seqs; ++q) segn[q] = row0[q + 1] - row0[q];
+        HIPTRY(c, hipMemcpyAsync(c->meta.p, mz.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->plen.p, pl.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        check_prefix(tokens, as<int32_t>(c->plen), n_seqs, c->T, c->V, as<int32_t>(c->meta) + kMetaError, s);
+        int32_t err = 0;
+        HIPTRY(c, hipMemcpyAsync(&err, as<int32_t>(c->meta) + kMetaError, 4, hipMemcpyDeviceToHost, s));
+        HIPTRY(c, hipStreamSynchronize(s));
+        if (err) return fail(HBSJD_EINVAL, "a token is outside [0, vocab)");
+        HIPTRY(c, hipMemcpyAsync(c->labels.p, lab.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seq_row0.p, row0.data(), (n_seqs + 1) * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seq_img.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seq_branch.p, sbr.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seg_seq.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, row0.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        std::vector<int32_t> mpf(kMetaCount, 0);
+        mpf[kMetaRows] = rows;
+        mpf[kMetaSegs] = n_seqs;
+        HIPTRY(c, hipMemcpyAsync(c->meta_pf.p, mpf.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+        HIPTRY(c, hipStreamSynchronize(s));
+        // C is the null class here; the row builder maps branch 0 to labels[b]
+        PrefillRowsArgs pa{n_seqs, c->T, 1, c->C, c->max_pages, rows, as<int32_t>(c->seq_row0),
+                           as<int32_t>(c->seq_img), as<int32_t>(c->seq_branch), tokens,
+                           as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->row_tok),
+                           as<int32_t>(c->row_pos), as<int32_t>(c->row_kv), as<int32_t>(c->row_seq)};
+        prefill_rows(pa, s);
+        int32_t* mp = as<int32_t>(c->meta_pf);
+        FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
+                           as<int32_t>(c->row_seq)},
+                   mp + kMetaRows, rows,
+                   Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0),
+                            as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0)},
+                   mp + kMetaSegs, n_seqs, maxlen};
+        forward_layers(c, fr);
+        rmsnorm(c->bf16, as<float>(c->h), nullptr, mp + kMetaRows, rows, c->g_out, c->m.rms_eps,
+                c->d, c->hb.p, s);
+        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaRows, rows, logits,
+                    c->b_lm, s);
+        HIPTRY(c, hipGetLastError());
+        HIPTRY(c, hipStreamSynchronize(s));
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_forward");
+    }
+}
+
+hbsjd_status hbsjd_verify_probs(int32_t B, int32_t W, int32_t V, const float* p, const float* q,
+                                const int32_t* drafts, const float* u_acc, const float* u_res,
+                                int32_t* counts, int32_t* tokens, void* stream) {
+    try {
+        if (B < 1 || W < 1 || V < 1 || V > kMaxVocab)
+            return fail(HBSJD_EINVAL, "need B >= 1, W >= 1, 1 <= V <= 16384");
+        if (!p || !q || !drafts || !u_acc || !u_res || !counts || !tokens)
+            return fail(HBSJD_EINVAL, "NULL buffer");
+        hipStream_t s = (hipStream_t)stream;
+        verify_probs(B, W, V, p, q, drafts, u_acc, u_res, counts, tokens, s);
+        hipError_t e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("verify_probs: ") + hipGetErrorString(e));
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_verify_probs");
+    }
+}
+
+hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t* out, void* stream) {
+    try {
+        if (n < 0 || (n > 0 && (!bt || !out))) return fail(HBSJD_EINVAL, "bad philox arguments");
+        hipStream_t s = (hipStream_t)stream;
+        philox_fill(seed, n, bt, out, s);
+        hipError_t e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("philox: ") + hipGetErrorString(e));
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_philox");
+    }
+}
+
+hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* c, int32_t batch, int32_t window, int32_t* gamma) {
+    (void)batch;
+    (void)window;
+    try {
+        GUARD(c);
+        if (!gamma) return fail(HBSJD_EINVAL, "gamma is NULL");
+        return fail(HBSJD_ESTATE, "calibration is not built yet");
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_calibrate_gamma");
+    }
+}
+
+}  // extern "C"

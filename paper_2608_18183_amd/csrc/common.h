@@ -1,0 +1,148 @@
+// Shared device helpers of the HIP library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hbsjd {
+
+// ------------------------------------------------------------ constants
+
+constexpr int kPage = 64;       // KV slots per page; also the attention key tile
+constexpr int kChunk = 64;      // vocabulary sums run sequentially inside 64-entry chunks
+constexpr int kMaxVocab = 16384;
+constexpr int kMaxChunks = kMaxVocab / kChunk;
+
+// per-round device bookkeeping written by the round set-up kernel (int32 slots)
+enum MetaSlot : int {
+    kMetaRows = 0,     // rows in the verifier forward (all CFG branches)
+    kMetaOutRows = 1,  // distribution rows (one per image and window row)
+    kMetaImgs = 2,     // images physically processed this round
+    kMetaSegs = 3,     // attention segments (one per sequence processed)
+    kMetaActive = 4,   // A: images that still have tokens to generate
+    kMetaMode = 5,     // 0 Full, 1 Compact
+    kMetaRound = 6,    // index of the round in progress
+    kMetaError = 7,    // sticky device error bits
+    kMetaCount = 16,
+};
+
+enum DeviceError : int {
+    kErrNanLogit = 1,
+    kErrZeroProposal = 2,
+    kErrBadToken = 4,
+    kErrRoundOverflow = 8,
+};
+
+// ------------------------------------------------------------ bf16
+
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+    uint32_t u;
+    __builtin_memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__host__ __device__ inline float bf16_to_f32(uint16_t h) {
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    __builtin_memcpy(&f, &u, 4);
+    return f;
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    __device__ static float load(const float* p) { return *p; }
+    __device__ static void store(float* p, float v) { *p = v; }
+};
+template <> struct Elem<uint16_t> {
+    __device__ static float load(const uint16_t* p) { return bf16_to_f32(*p); }
+    __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+// ------------------------------------------------------------ Philox4x32-10
+
+// Counter-based generator of Salmon, Moraes, Dror and Shaw (SC'11): ten
+// rounds of the two-multiply bijection, the key bumped by the Weyl constants
+// between rounds.
+struct U4 { uint32_t x, y, z, w; };
+
+__host__ __device__ inline U4 philox4x32_10(uint64_t seed, uint32_t c0, uint32_t c1,
+                                            uint32_t c2, uint32_t c3) {
+    uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t m0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t m1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
+        const uint32_t n1 = (uint32_t)m1;
+        const uint32_t n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+        const uint32_t n3 = (uint32_t)m0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return U4{c0, c1, c2, c3};
+}
+
+// uniform on [0, 1 - 2^-24] from the 24 high bits
+__host__ __device__ inline float unit_float(uint32_t x) {
+    return (float)(x >> 8) * (1.0f / 16777216.0f);
+}
+
+// the three uniforms of image b at sequence position t: draft, accept, resample
+struct Uniforms { float draft, acc, res; };
+__device__ inline Uniforms uniforms_at(uint64_t seed, int b, int t) {
+    const U4 o = philox4x32_10(seed, (uint32_t)b, (uint32_t)t, 0u, 0u);
+    return Uniforms{unit_float(o.x), unit_float(o.y), unit_float(o.z)};
+}
+
+// ------------------------------------------------------------ reductions
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ inline float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ inline float wave_min(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ inline int wave_min_int(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ inline int wave_max_int(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ inline int wave_sum_int(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// block-wide reductions for 256-thread blocks (fixed tree order)
+template <typename F>
+__device__ inline float block_reduce(float v, float* red, F op) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = op(v, __shfl_xor(v, o, 64));
+    __syncthreads();
+    if (lane == 0) red[wid] = v;
+    __syncthreads();
+    float r = op(op(red[0], red[1]), op(red[2], red[3]));
+    __syncthreads();
+    return r;
+}
+
+}  // namespace hbsjd

@@ -1,0 +1,149 @@
+// Host-side launchers of the library's kernels (internal interface).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hbsjd {
+
+// The paged KV cache of one layer is an array of pages of 64 slots; page p
+// holds, for every head h, K as [64 slots][head_dim] at
+// (p * 2 * heads + h) * 64 * head_dim and V transposed as [head_dim][64 slots]
+// at (p * 2 * heads + heads + h) * 64 * head_dim. A sequence's page table maps
+// its tile j (positions 64 j .. 64 j + 63) to a page.
+
+// Per-row metadata of a verifier (or prefill) forward.
+struct RowMeta {
+    const int32_t* tok;   // token id, or -(1 + class) for the class embedding
+    const int32_t* pos;   // sequence position
+    const int32_t* kv;    // page * 64 + slot of the row's KV entry
+    const int32_t* seq;   // sequence (image * cfg + branch)
+};
+
+// Attention segments: consecutive rows of one sequence at consecutive positions.
+struct Segments {
+    const int32_t* seq;
+    const int32_t* row0;
+    const int32_t* nrows;
+    const int32_t* pos0;
+};
+
+// ---------------------------------------------------------------- GEMM
+// C[M x N] = A[M x K] . W[N x K]^T with a fused epilogue. M is read from
+// m_dev (clamped to m_cap) when m_dev is not null; the grid covers m_cap rows.
+
+struct QkvArgs {
+    void* q;              // [M][d] activation dtype
+    void* kv;             // layer base of the KV pool
+    const int32_t* pos;
+    const int32_t* kvslot;
+    const float* rope_cos;   // [(T+1)][dh/2]
+    const float* rope_sin;
+    int d, heads, head_dim, T;
+};
+
+void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
+              int m_cap, const QkvArgs& e, hipStream_t s);
+void gemm_residual(bool bf16, const void* A, int lda, const void* W, int N, int K,
+                   const int* m_dev, int m_cap, float* h, hipStream_t s);
+void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
+                 const int* m_dev, int m_cap, void* act, hipStream_t s);
+void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
+                 const int* m_dev, int m_cap, float* out, const float* bias, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+void attention(bool bf16, const void* q, void* o, int d, int heads, int head_dim,
+               const void* kv_layer, const int32_t* ptab, int max_pages, const Segments& seg,
+               const int* nseg_dev, int nseg_cap, int max_rows_per_seg, const RowMeta& rows,
+               const int* nrows_dev, int nrows_cap, hipStream_t s);
+
+// ---------------------------------------------------------------- row ops
+void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
+                const void* tok_emb, const void* cls_emb, const float* gain, float eps, int d,
+                float* h, void* hb, hipStream_t s);
+void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
+             int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s);
+
+struct RoundSetupArgs {
+    int B, W, T, cfg, C, gamma, exec_mode, max_pages, max_rounds;
+    const int32_t* cursor;
+    const int32_t* drafts;
+    const int32_t* xtok;
+    const int32_t* labels;
+    const int32_t* ptab;
+    int32_t* slot_img;
+    int32_t* active_list;
+    int32_t* row_tok;
+    int32_t* row_pos;
+    int32_t* row_kv;
+    int32_t* row_seq;
+    int32_t* seg_seq;
+    int32_t* seg_row0;
+    int32_t* seg_nrows;
+    int32_t* seg_pos0;
+    int32_t* meta;
+    int32_t* a_hist;
+    int32_t* mode_hist;
+};
+void round_setup(const RoundSetupArgs& a, hipStream_t s);
+
+struct PrefillRowsArgs {
+    int n_seq, T, cfg, C, max_pages, total_rows;
+    const int32_t* seq_row0;     // [n_seq + 1]
+    const int32_t* seq_img;      // [n_seq]
+    const int32_t* seq_branch;   // [n_seq]
+    const int32_t* prefix;       // device [B][T]
+    const int32_t* labels;       // device [B]
+    const int32_t* ptab;
+    int32_t* row_tok;
+    int32_t* row_pos;
+    int32_t* row_kv;
+    int32_t* row_seq;
+};
+void prefill_rows(const PrefillRowsArgs& a, hipStream_t s);
+void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V, int32_t* err,
+                  hipStream_t s);
+void philox_fill(uint64_t seed, int n, const uint32_t* bt, uint32_t* out, hipStream_t s);
+
+// ---------------------------------------------------------------- sampler
+struct TransformArgs {
+    const float* logits;     // forward rows [rows][V]
+    float* p;                // distribution rows [out][V] (may equal logits without CFG)
+    float* cprefix;          // [out][nchunks + 1]
+    int32_t* amax;           // [out]
+    const int32_t* slot_img;
+    const float* temperature;   // [B]
+    int rows_per_slot, cfg, V, top_k;
+    float cfg_scale;
+    const int* nout_dev;
+    int nout_cap;
+    int32_t* meta;
+};
+void transform(const TransformArgs& a, hipStream_t s);
+
+struct VerifyArgs {
+    int B, W, T, H, V, greedy, prefill, rows_per_slot, max_rounds;
+    uint64_t seed;
+    const float* p;          // this round's distribution rows
+    const float* cprefix;
+    const int32_t* amax;
+    const float* p_prev;     // previous round's rows (proposals)
+    const int32_t* slot_img;
+    const int* nimg_dev;
+    int nimg_cap;
+    int32_t* cursor;
+    int32_t* xtok;
+    int32_t* drafts;
+    int32_t* qsrc;
+    int32_t* counts;         // [max_rounds][B] or null
+    int64_t* stats;          // [4]
+    int32_t* meta;
+};
+void verify_commit(const VerifyArgs& a, hipStream_t s);
+
+void verify_probs(int B, int W, int V, const float* p, const float* q, const int32_t* drafts,
+                  const float* u_acc, const float* u_res, int32_t* counts, int32_t* tokens,
+                  hipStream_t s);
+
+}  // namespace hbsjd

@@ -1,0 +1,234 @@
+// Row bookkeeping of the rollout: per-round active compaction and execution
+// mode (Sec. 4.3, Eq. 6), verifier-row assembly (last committed token followed
+// by the draft window at per-image positions and KV slots, Sec. 4.2), prefill
+// rows, the embedding gather, and RMSNorm.
+#include "common.h"
+#include "launch.h"
+
+namespace hbsjd {
+
+// ---------------------------------------------------------------- round set-up
+// One workgroup. Prefix-scan of active flags (n_b < T) gives A and the ordered
+// list of active images; Full processes every image (finished ones computed
+// and discarded), Compact only the active list. Then writes the row metadata
+// of the chosen images: row (slot, branch, i) holds position n_b + i with token
+// x_{n_b} (class token when n_b = 0) for i = 0 and draft i otherwise.
+__global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
+    __shared__ int warp_tot[16];
+    __shared__ int s_base;
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    if (t == 0) s_base = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < a.B; c0 += 1024) {
+        const int b = c0 + t;
+        const int act = (b < a.B && a.cursor[b] < a.T) ? 1 : 0;
+        // inclusive scan inside the wave
+        int x = act;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+        }
+        if (lane == 63) warp_tot[wv] = x;
+        __syncthreads();
+        int before = s_base;
+        for (int k = 0; k < wv; ++k) before += warp_tot[k];
+        if (act) a.active_list[before + x - 1] = b;
+        __syncthreads();
+        if (t == 0) {
+            int s = s_base;
+            for (int k = 0; k < 16; ++k) s += warp_tot[k];
+            s_base = s;
+        }
+        __syncthreads();
+    }
+    const int A = s_base;
+    int mode;
+    if (a.exec_mode == 1) mode = 0;
+    else if (a.exec_mode == 2) mode = 1;
+    else mode = A > a.gamma ? 0 : 1;
+    const int nimg = A == 0 ? 0 : (mode == 0 ? a.B : A);
+    const int R = a.W + 1;
+    const int rows = nimg * a.cfg * R;
+    for (int s = t; s < nimg; s += 1024) a.slot_img[s] = mode == 0 ? s : a.active_list[s];
+    __syncthreads();
+    for (int r = t; r < rows; r += 1024) {
+        const int s = r / (a.cfg * R);
+        const int rem = r - s * a.cfg * R;
+        const int br = rem / R, i = rem - br * R;
+        const int b = a.slot_img[s];
+        int n = a.cursor[b];
+        n = n > a.T ? a.T : n;
+        const int We = min(a.W, a.T - n);
+        const int seq = b * a.cfg + br;
+        const int pos = n + i;
+        int tok;
+        if (i == 0)
+            tok = n == 0 ? -(1 + (br == 0 ? a.labels[b] : a.C)) : a.xtok[(size_t)b * a.T + n - 1];
+        else
+            tok = i <= We ? a.drafts[(size_t)b * a.W + i - 1] : 0;
+        a.row_tok[r] = tok;
+        a.row_pos[r] = pos;
+        a.row_seq[r] = seq;
+        a.row_kv[r] = a.ptab[(size_t)seq * a.max_pages + (pos >> 6)] * 64 + (pos & 63);
+    }
+    for (int q = t; q < nimg * a.cfg; q += 1024) {
+        const int s = q / a.cfg, br = q - s * a.cfg;
+        const int b = a.slot_img[s];
+        int n = a.cursor[b];
+        n = n > a.T ? a.T : n;
+        a.seg_seq[q] = b * a.cfg + br;
+        a.seg_row0[q] = q * R;
+        a.seg_nrows[q] = R;
+        a.seg_pos0[q] = n;
+    }
+    if (t == 0) {
+        const int round = a.meta[kMetaRound] + 1;
+        a.meta[kMetaRound] = round;
+        a.meta[kMetaRows] = rows;
+        a.meta[kMetaOutRows] = nimg * R;
+        a.meta[kMetaImgs] = nimg;
+        a.meta[kMetaSegs] = nimg * a.cfg;
+        a.meta[kMetaActive] = A;
+        a.meta[kMetaMode] = mode;
+        if (round < a.max_rounds) {
+            a.a_hist[round] = A;
+            a.mode_hist[round] = mode;
+        } else if (A > 0) {
+            atomicOr(&a.meta[kMetaError], (int)kErrRoundOverflow);
+        }
+    }
+}
+
+void round_setup(const RoundSetupArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(k_round_setup, dim3(1), dim3(1024), 0, s, a);
+}
+
+// ---------------------------------------------------------------- prefill rows
+// row r of sequence q (image b, branch br) is position r - seq_row0[q]: the
+// class token at 0, prefix token x_p at p >= 1.
+__global__ void k_prefill_rows(PrefillRowsArgs a) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.total_rows) return;
+    int lo = 0, hi = a.n_seq;   // find q with seq_row0[q] <= r < seq_row0[q+1]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (a.seq_row0[mid] <= r) lo = mid; else hi = mid;
+    }
+    const int q = lo;
+    const int b = a.seq_img[q], br = a.seq_branch[q];
+    const int pos = r - a.seq_row0[q];
+    const int seq = b * a.cfg + br;
+    a.row_tok[r] = pos == 0 ? -(1 + (br == 0 ? a.labels[b] : a.C))
+                            : a.prefix[(size_t)b * a.T + pos - 1];
+    a.row_pos[r] = pos;
+    a.row_seq[r] = seq;
+    a.row_kv[r] = a.ptab[(size_t)seq * a.max_pages + (pos >> 6)] * 64 + (pos & 63);
+}
+
+void prefill_rows(const PrefillRowsArgs& a, hipStream_t s) {
+    if (a.total_rows <= 0) return;
+    hipLaunchKernelGGL(k_prefill_rows, dim3((a.total_rows + 255) / 256), dim3(256), 0, s, a);
+}
+
+__global__ void k_check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V,
+                               int32_t* err) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= B * T) return;
+    const int b = i / T, t = i - b * T;
+    if (t < len[b]) {
+        const int v = prefix[i];
+        if (v < 0 || v >= V) atomicOr(err, (int)kErrBadToken);
+    }
+}
+
+void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V, int32_t* err,
+                  hipStream_t s) {
+    const int n = B * T;
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_check_prefix, dim3((n + 255) / 256), dim3(256), 0, s, prefix, len, B, T,
+                       V, err);
+}
+
+// ---------------------------------------------------------------- norms
+// RMSNorm(x) * g = x * (1 / sqrt(mean(x^2) + eps)) * g, one 256-thread block per row.
+
+template <typename T>
+__device__ inline void norm_row(const float* x, const float* g, float eps, int d, T* out,
+                                float* red) {
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(x[i], x[i], ss);
+    ss = block_reduce(ss, red, [](float u, float v) { return u + v; });
+    const float r = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int i = threadIdx.x; i < d; i += 256) Elem<T>::store(out + i, (x[i] * r) * g[i]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nrows_dev,
+                                                    const T* tok_emb, const T* cls_emb,
+                                                    const float* g, float eps, int d, float* h,
+                                                    T* hb) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    if (r >= *nrows_dev) return;
+    const int tok = rows.tok[r];
+    const T* e = tok >= 0 ? tok_emb + (size_t)tok * d : cls_emb + (size_t)(-(tok + 1)) * d;
+    float* hr = h + (size_t)r * d;
+    for (int i = threadIdx.x; i < d; i += 256) hr[i] = Elem<T>::load(e + i);
+    __syncthreads();
+    norm_row(hr, g, eps, d, hb + (size_t)r * d, red);
+}
+
+void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
+                const void* tok_emb, const void* cls_emb, const float* gain, float eps, int d,
+                float* h, void* hb, hipStream_t s) {
+    if (nrows_cap <= 0) return;
+    if (bf16)
+        hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, rows,
+                           nrows_dev, (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain,
+                           eps, d, h, (uint16_t*)hb);
+    else
+        hipLaunchKernelGGL(k_embed_norm<float>, dim3(nrows_cap), dim3(256), 0, s, rows, nrows_dev,
+                           (const float*)tok_emb, (const float*)cls_emb, gain, eps, d, h,
+                           (float*)hb);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* h, const int32_t* src_idx,
+                                                 const int* nrows_dev, const float* g, float eps,
+                                                 int d, T* hb) {
+    __shared__ float red[4];
+    const int r = blockIdx.x;
+    if (r >= *nrows_dev) return;
+    const int src = src_idx ? src_idx[r] : r;
+    norm_row(h + (size_t)src * d, g, eps, d, hb + (size_t)r * d, red);
+}
+
+void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
+             int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s) {
+    if (nrows_cap <= 0) return;
+    if (bf16)
+        hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
+                           nrows_dev, gain, eps, d, (uint16_t*)hb);
+    else
+        hipLaunchKernelGGL(k_rmsnorm<float>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
+                           nrows_dev, gain, eps, d, (float*)hb);
+}
+
+// ---------------------------------------------------------------- Philox test entry
+__global__ void k_philox(uint64_t seed, int n, const uint32_t* bt, uint32_t* out) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const U4 r = philox4x32_10(seed, bt[2 * i], bt[2 * i + 1], 0u, 0u);
+    out[4 * i + 0] = r.x;
+    out[4 * i + 1] = r.y;
+    out[4 * i + 2] = r.z;
+    out[4 * i + 3] = r.w;
+}
+
+void philox_fill(uint64_t seed, int n, const uint32_t* bt, uint32_t* out, hipStream_t s) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_philox, dim3((n + 255) / 256), dim3(256), 0, s, seed, n, bt, out);
+}
+
+}  // namespace hbsjd

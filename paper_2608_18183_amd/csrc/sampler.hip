@@ -1,0 +1,560 @@
+// Sampling side of a round: the distribution transform of every verifier row,
+// probabilistic (Sec. 4.2, Eq. 5) or greedy (Eq. 4) verification of each
+// image's window, commit, and the Jacobi window refresh (reused predictions
+// first, history tokens at offset H for the rest; Sec. 4.2).
+//
+// Every fp32 sum over the vocabulary is associated the same way: sequential
+// inside consecutive 64-entry chunks, then the chunk totals sequential. The
+// inverse CDF returns the first entry whose prefix (chunk prefix plus in-chunk
+// prefix) exceeds u * total. Contraction is off in this file so each operation
+// rounds once.
+#include "common.h"
+#include "launch.h"
+
+#pragma clang fp contract(off)
+
+namespace hbsjd {
+
+constexpr int kBins = 1024;     // histogram bins of the top-k threshold search
+constexpr int kCand = 256;      // candidates ranked exactly once the bin is this small
+
+// ---------------------------------------------------------------- transform
+// One 256-thread block per distribution row; thread c owns vocabulary chunk c
+// (64 consecutive entries) in registers.
+__global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
+    __shared__ float red[4];
+    __shared__ int ired[8];
+    __shared__ int hist[kBins];
+    __shared__ float tot[kMaxChunks + 1];
+    __shared__ float cand[kCand];
+    __shared__ int s_int[4];
+    __shared__ float s_flt[4];
+
+    const int r = blockIdx.x;
+    if (r >= min(*a.nout_dev, a.nout_cap)) return;
+    const int t = threadIdx.x;
+    const int V = a.V;
+    const int nC = (V + kChunk - 1) / kChunk;
+    const int s = r / a.rows_per_slot, i = r - s * a.rows_per_slot;
+    const int b = a.slot_img[s];
+    const float tau = a.temperature[b];
+    const float* lc = a.logits + (size_t)((s * a.cfg) * a.rows_per_slot + i) * V;
+    const float* lu = a.cfg == 2 ? a.logits + (size_t)((s * 2 + 1) * a.rows_per_slot + i) * V : nullptr;
+
+    // guided logits, temperature, max and argmax (of the guided logits)
+    float y[kChunk];
+    float lmax = -INFINITY, ymax = -INFINITY, ymin = INFINITY;
+    int lidx = 0x7fffffff;
+    int nan_seen = 0;
+    const int v0 = t * kChunk;
+#pragma unroll
+    for (int k = 0; k < kChunk; k += 4) {
+        float4 c4 = make_float4(0.f, 0.f, 0.f, 0.f), u4 = c4;
+        const bool in = v0 + k < V;
+        if (in) {
+            c4 = *reinterpret_cast<const float4*>(lc + v0 + k);
+            if (lu) u4 = *reinterpret_cast<const float4*>(lu + v0 + k);
+        }
+        const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
+        const float uv[4] = {u4.x, u4.y, u4.z, u4.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int v = v0 + k + q;
+            float l = cv[q];
+            if (lu) l = uv[q] + a.cfg_scale * (cv[q] - uv[q]);
+            const float yy = l / tau;
+            y[k + q] = yy;
+            if (v < V) {
+                if (l != l) nan_seen = 1;
+                if (l > lmax) { lmax = l; lidx = v; }
+                ymax = fmaxf(ymax, yy);
+                ymin = fminf(ymin, yy);
+            }
+        }
+    }
+    if (nan_seen) atomicOr(&a.meta[kMetaError], (int)kErrNanLogit);
+    // argmax with the lowest index on ties
+    {
+        float m = lmax;
+        int idx = lidx;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const float m2 = __shfl_xor(m, o, 64);
+            const int i2 = __shfl_xor(idx, o, 64);
+            if (m2 > m || (m2 == m && i2 < idx)) { m = m2; idx = i2; }
+        }
+        if ((t & 63) == 0) { red[t >> 6] = m; ired[t >> 6] = idx; }
+        __syncthreads();
+        if (t == 0) {
+            float bm = red[0];
+            int bi = ired[0];
+            for (int w = 1; w < 4; ++w)
+                if (red[w] > bm || (red[w] == bm && ired[w] < bi)) { bm = red[w]; bi = ired[w]; }
+            a.amax[r] = bi;
+        }
+        __syncthreads();
+    }
+    ymax = block_reduce(ymax, red, [](float p, float q) { return fmaxf(p, q); });
+
+    // top-k threshold: the k-th largest y counting ties (exact)
+    float thr = -INFINITY;
+    if (a.top_k > 0 && a.top_k < V) {
+        ymin = block_reduce(ymin, red, [](float p, float q) { return fminf(p, q); });
+        float lo = ymin, hi = ymax;
+        int above = 0;   // entries strictly above the current range
+        for (int iter = 0; iter < 64; ++iter) {
+            if (lo == hi) { thr = lo; break; }
+            for (int k = t; k < kBins; k += 256) hist[k] = 0;
+            __syncthreads();
+            const float scale = (float)kBins / (hi - lo);
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k) {
+                const float yy = y[k];
+                if (v0 + k < V && yy >= lo && yy <= hi) {
+                    int bin = (int)((yy - lo) * scale);
+                    bin = bin > kBins - 1 ? kBins - 1 : bin;
+                    atomicAdd(&hist[bin], 1);
+                }
+            }
+            __syncthreads();
+            // suffix counts: thread t owns bins 4t..4t+3
+            int own = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) own += hist[4 * t + q];
+            // inclusive suffix scan over threads (higher threads = higher bins)
+            int sfx = own;
+            {
+                const int lane = t & 63, wv = t >> 6;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int yv = __shfl_down(sfx, o, 64);
+                    if (lane + o < 64) sfx += yv;
+                }
+                if (lane == 0) ired[wv] = sfx;
+                __syncthreads();
+                for (int w = wv + 1; w < 4; ++w) sfx += ired[w];
+                __syncthreads();
+            }
+            // entries in bins above thread t's group
+            int cum = above + sfx - own;
+            if (t == 0) {
+                s_int[0] = -1;
+                s_int[1] = 0;
+                s_int[2] = 0;
+            }
+            __syncthreads();
+            for (int q = 3; q >= 0; --q) {
+                const int hb = hist[4 * t + q];
+                if (cum < a.top_k && a.top_k <= cum + hb) {
+                    s_int[0] = 4 * t + q;
+                    s_int[1] = cum;
+                    s_int[2] = hb;
+                }
+                cum += hb;
+            }
+            __syncthreads();
+            const int bstar = s_int[0];
+            const int above_new = s_int[1];
+            const int cnt = s_int[2];
+            __syncthreads();
+            if (bstar < 0) {   // only with NaN logits, which are reported as an error
+                thr = lo;
+                break;
+            }
+            if (cnt <= kCand) {
+                if (t == 0) s_int[3] = 0;
+                __syncthreads();
+#pragma unroll
+                for (int k = 0; k < kChunk; ++k) {
+                    const float yy = y[k];
+                    if (v0 + k < V && yy >= lo && yy <= hi) {
+                        int bin = (int)((yy - lo) * scale);
+                        bin = bin > kBins - 1 ? kBins - 1 : bin;
+                        if (bin == bstar) cand[atomicAdd(&s_int[3], 1)] = yy;
+                    }
+                }
+                __syncthreads();
+                const int need = a.top_k - above_new;   // rank inside the bin, 1-based
+                if (t < cnt) {
+                    const float cv = cand[t];
+                    int gt = 0, ge = 0;
+                    for (int j = 0; j < cnt; ++j) {
+                        gt += cand[j] > cv;
+                        ge += cand[j] >= cv;
+                    }
+                    if (gt < need && need <= ge) s_flt[0] = cv;
+                }
+                __syncthreads();
+                thr = s_flt[0];
+                break;
+            }
+            // narrow to the values that fell into the chosen bin
+            float blo = INFINITY, bhi = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k) {
+                const float yy = y[k];
+                if (v0 + k < V && yy >= lo && yy <= hi) {
+                    int bin = (int)((yy - lo) * scale);
+                    bin = bin > kBins - 1 ? kBins - 1 : bin;
+                    if (bin == bstar) { blo = fminf(blo, yy); bhi = fmaxf(bhi, yy); }
+                }
+            }
+            blo = block_reduce(blo, red, [](float p, float q) { return fminf(p, q); });
+            bhi = block_reduce(bhi, red, [](float p, float q) { return fmaxf(p, q); });
+            lo = blo;
+            hi = bhi;
+            above = above_new;
+            thr = lo;   // only reached if the loop runs out: keeps at least k entries
+        }
+    }
+
+    // softmax over the kept entries; Z in the pinned chunk order
+    float csum = 0.f;
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k) {
+        const float e = (v0 + k < V && y[k] >= thr) ? expf(y[k] - ymax) : 0.f;
+        y[k] = e;
+        csum = csum + e;
+    }
+    if (t < nC) tot[t] = csum;
+    __syncthreads();
+    if (t == 0) {
+        float z = 0.f;
+        for (int c = 0; c < nC; ++c) z = z + tot[c];
+        s_flt[1] = z;
+    }
+    __syncthreads();
+    const float z = s_flt[1];
+    float* prow = a.p + (size_t)r * V;
+    float psum = 0.f;
+#pragma unroll
+    for (int k = 0; k < kChunk; k += 4) {
+        float pv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pv[q] = y[k + q] / z;
+            psum = psum + pv[q];
+        }
+        if (v0 + k < V) *reinterpret_cast<float4*>(prow + v0 + k) = make_float4(pv[0], pv[1], pv[2], pv[3]);
+    }
+    __syncthreads();
+    if (t < nC) tot[t] = psum;
+    __syncthreads();
+    if (t == 0) {
+        float* cp = a.cprefix + (size_t)r * (nC + 1);
+        float run = 0.f;
+        cp[0] = 0.f;
+        for (int c = 0; c < nC; ++c) {
+            run = run + tot[c];
+            cp[c + 1] = run;
+        }
+    }
+}
+
+void transform(const TransformArgs& a, hipStream_t s) {
+    if (a.nout_cap <= 0) return;
+    hipLaunchKernelGGL(k_transform, dim3(a.nout_cap), dim3(256), 0, s, a);
+}
+
+// ---------------------------------------------------------------- inverse CDF helpers
+
+// Wave-level draw from a distribution row with its chunk prefix cp[0..nC].
+__device__ inline int wave_sample_cp(const float* prow, const float* cp, int V, int nC, float u) {
+    const int lane = threadIdx.x & 63;
+    const float target = u * cp[nC];
+    int cs = 0x7fffffff;
+    for (int c = lane; c < nC; c += 64)
+        if (cp[c + 1] > target) { cs = c; break; }
+    cs = wave_min_int(cs);
+    if (cs == 0x7fffffff) {
+        int last = -1;
+        for (int v = lane; v < V; v += 64)
+            if (prow[v] > 0.f) last = v;
+        return wave_max_int(last);
+    }
+    const int v = cs * kChunk + lane;
+    const float pv = v < V ? prow[v] : 0.f;
+    const float before = cp[cs];
+    float inner = 0.f;
+    int found = -1, lastpos = -1;
+    for (int k = 0; k < kChunk; ++k) {
+        const float x = __shfl(pv, k, 64);
+        if (cs * kChunk + k >= V) break;
+        inner = inner + x;
+        if (x > 0.f) lastpos = cs * kChunk + k;
+        if (before + inner > target) { found = cs * kChunk + k; break; }
+    }
+    return found >= 0 ? found : lastpos;
+}
+
+// Block-level draw from non-negative weights w(v) computed on the fly; returns
+// -1 when every weight is zero. All 256 threads must call it.
+template <typename F>
+__device__ int block_inv_cdf(F w, int V, float u, float* cp, int* res) {
+    const int t = threadIdx.x;
+    const int nC = (V + kChunk - 1) / kChunk;
+    for (int c = t; c < nC; c += 256) {
+        float sum = 0.f;
+        for (int k = 0; k < kChunk; ++k) {
+            const int v = c * kChunk + k;
+            if (v < V) sum = sum + w(v);
+        }
+        cp[c + 1] = sum;
+    }
+    __syncthreads();
+    if (t == 0) {
+        float run = 0.f;
+        cp[0] = 0.f;
+        for (int c = 0; c < nC; ++c) {
+            run = run + cp[c + 1];
+            cp[c + 1] = run;
+        }
+    }
+    __syncthreads();
+    const float total = cp[nC];
+    if (!(total > 0.f)) return -1;
+    if (t < 64) {
+        const int lane = t;
+        const float target = u * total;
+        int cs = 0x7fffffff;
+        for (int c = lane; c < nC; c += 64)
+            if (cp[c + 1] > target) { cs = c; break; }
+        cs = wave_min_int(cs);
+        int out;
+        if (cs == 0x7fffffff) {
+            int last = -1;
+            for (int v = lane; v < V; v += 64)
+                if (w(v) > 0.f) last = v;
+            out = wave_max_int(last);
+        } else {
+            const int v = cs * kChunk + lane;
+            const float pv = v < V ? w(v) : 0.f;
+            const float before = cp[cs];
+            float inner = 0.f;
+            int found = -1, lastpos = -1;
+            for (int k = 0; k < kChunk; ++k) {
+                const float x = __shfl(pv, k, 64);
+                if (cs * kChunk + k >= V) break;
+                inner = inner + x;
+                if (x > 0.f) lastpos = cs * kChunk + k;
+                if (before + inner > target) { found = cs * kChunk + k; break; }
+            }
+            out = found >= 0 ? found : lastpos;
+        }
+        if (lane == 0) *res = out;
+    }
+    __syncthreads();
+    return *res;
+}
+
+// ---------------------------------------------------------------- verify + commit + refresh
+// One 256-thread block per processed image.
+__global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
+    __shared__ float cp[kMaxChunks + 1];
+    __shared__ int s_res;
+    __shared__ int s_first;
+    __shared__ int old_dr[64], old_q[64];
+    __shared__ int new_dr[64], new_q[64];
+
+    const int sl = blockIdx.x;
+    if (sl >= min(*a.nimg_dev, a.nimg_cap)) return;
+    const int t = threadIdx.x;
+    const int b = a.slot_img[sl];
+    const int n = a.cursor[b];
+    if (n >= a.T) return;              // finished image in Full mode: rows discarded
+    const int W = a.W, V = a.V, R = a.rows_per_slot;
+    const int nC = (V + kChunk - 1) / kChunk;
+    int n_new, base, nrows;
+    if (a.prefill) {
+        n_new = n;
+        base = n;
+        nrows = 1;
+    } else {
+        const int We = min(W, a.T - n);
+        if (t < W) {
+            old_dr[t] = a.drafts[(size_t)b * W + t];
+            old_q[t] = a.qsrc[(size_t)b * W + t];
+        }
+        if (t == 0) s_first = We + 1;
+        __syncthreads();
+        if (t < We) {
+            const int j = t + 1;
+            const int z = old_dr[t];
+            const int prow = sl * R + (j - 1);
+            bool acc;
+            if (a.greedy) {
+                acc = z == a.amax[prow];
+            } else {
+                const float P = a.p[(size_t)prow * V + z];
+                const int qs = old_q[t];
+                const float Q = qs >= 0 ? a.p_prev[(size_t)qs * V + z] : 1.0f;
+                if (!(Q > 0.f)) atomicOr(&a.meta[kMetaError], (int)kErrZeroProposal);
+                const float u = uniforms_at(a.seed, b, n + j).acc;
+                acc = (P >= Q) || (u < P / Q);
+            }
+            if (!acc) atomicMin(&s_first, j);
+        }
+        __syncthreads();
+        const int js = s_first;
+        const bool rejected = js <= We;
+        const int count = rejected ? js : We;
+        int rep = 0;
+        if (rejected) {
+            const int prow = sl * R + (js - 1);
+            if (a.greedy) {
+                rep = a.amax[prow];
+            } else {
+                const float* pr = a.p + (size_t)prow * V;
+                const int qs = old_q[js - 1];
+                const int z = old_dr[js - 1];
+                const float* qr = qs >= 0 ? a.p_prev + (size_t)qs * V : nullptr;
+                const float u = uniforms_at(a.seed, b, n + js).res;
+                rep = block_inv_cdf(
+                    [=](int v) {
+                        const float qv = qr ? qr[v] : (v == z ? 1.0f : 0.0f);
+                        const float d = pr[v] - qv;
+                        return d > 0.f ? d : 0.f;
+                    },
+                    V, u, cp, &s_res);
+                if (rep < 0) {
+                    if (t < 64) {
+                        const int got = wave_sample_cp(pr, a.cprefix + (size_t)prow * (nC + 1), V, nC, u);
+                        if (t == 0) s_res = got;
+                    }
+                    __syncthreads();
+                    rep = s_res;
+                }
+            }
+        }
+        // commit x_{n+1..n+count}
+        if (t < count) {
+            const int tok = (t == count - 1 && rejected) ? rep : old_dr[t];
+            a.xtok[(size_t)b * a.T + n + t] = tok;
+        }
+        if (t == 0) {
+            const int round = a.meta[kMetaRound];
+            if (a.counts && round >= 0 && round < a.max_rounds) a.counts[(size_t)round * a.B + b] = count;
+            atomicAdd((unsigned long long*)&a.stats[0], (unsigned long long)count);
+            atomicAdd((unsigned long long*)&a.stats[1], (unsigned long long)(rejected ? 1 : 0));
+            atomicAdd((unsigned long long*)&a.stats[2], 1ull);
+            a.cursor[b] = n + count;
+        }
+        n_new = n + count;
+        base = n;
+        nrows = We + 1;
+        __syncthreads();
+    }
+    // refresh the window for positions n_new+1 .. n_new+span
+    if (n_new >= a.T) {
+        if (t < W) {
+            a.drafts[(size_t)b * W + t] = -1;
+            a.qsrc[(size_t)b * W + t] = -1;
+        }
+        return;
+    }
+    const int span = min(W, a.T - n_new);
+    const int reused = min(span, base + nrows - n_new);   // positions covered by this round's rows
+    const int lane = t & 63, wv = t >> 6;
+    for (int m = 1 + wv; m <= reused; m += 4) {
+        const int pos = n_new + m;
+        const int i = pos - base - 1;
+        const int prow = sl * R + i;
+        int z;
+        if (a.greedy)
+            z = a.amax[prow];
+        else
+            z = wave_sample_cp(a.p + (size_t)prow * V, a.cprefix + (size_t)prow * (nC + 1), V, nC,
+                               uniforms_at(a.seed, b, pos).draft);
+        if (lane == 0) {
+            new_dr[m - 1] = z;
+            new_q[m - 1] = prow;
+        }
+    }
+    __syncthreads();
+    if (t == 0) {
+        for (int m = reused + 1; m <= span; ++m) {
+            const int pos = n_new + m;
+            const int src = pos - a.H >= 1 ? pos - a.H : pos - 1;
+            new_dr[m - 1] = src <= n_new ? a.xtok[(size_t)b * a.T + src - 1] : new_dr[src - n_new - 1];
+            new_q[m - 1] = -1;
+        }
+    }
+    __syncthreads();
+    if (t < W) {
+        a.drafts[(size_t)b * W + t] = t < span ? new_dr[t] : -1;
+        a.qsrc[(size_t)b * W + t] = t < span ? new_q[t] : -1;
+    }
+}
+
+void verify_commit(const VerifyArgs& a, hipStream_t s) {
+    if (a.nimg_cap <= 0) return;
+    hipLaunchKernelGGL(k_verify, dim3(a.nimg_cap), dim3(256), 0, s, a);
+}
+
+// ---------------------------------------------------------------- explicit-row verification
+__global__ __launch_bounds__(256) void k_verify_probs(int W, int V, const float* p, const float* q,
+                                                      const int32_t* drafts, const float* u_acc,
+                                                      const float* u_res, int32_t* counts,
+                                                      int32_t* tokens) {
+    __shared__ float cp[kMaxChunks + 1];
+    __shared__ int s_res, s_first;
+    __shared__ int s_bad;
+    const int b = blockIdx.x, t = threadIdx.x;
+    if (t == 0) {
+        s_first = W + 1;
+        s_bad = 0;
+    }
+    __syncthreads();
+    for (int j = t; j < W; j += 256) {
+        const int z = drafts[(size_t)b * W + j];
+        if (z < 0 || z >= V) s_bad = 1;
+    }
+    __syncthreads();
+    if (s_bad) {
+        for (int j = t; j < W; j += 256) tokens[(size_t)b * W + j] = -1;
+        if (t == 0) counts[b] = 0;
+        return;
+    }
+    for (int j = t; j < W; j += 256) {
+        const size_t row = (size_t)b * W + j;
+        const int z = drafts[row];
+        const float P = p[row * V + z];
+        const float Q = q[row * V + z];
+        const bool acc = (P >= Q) || (u_acc[row] < P / Q);
+        if (!acc) atomicMin(&s_first, j + 1);
+    }
+    __syncthreads();
+    const int js = s_first;
+    const bool rejected = js <= W;
+    const int count = rejected ? js : W;
+    int rep = 0;
+    if (rejected) {
+        const float* pr = p + ((size_t)b * W + js - 1) * V;
+        const float* qr = q + ((size_t)b * W + js - 1) * V;
+        const float u = u_res[b];
+        rep = block_inv_cdf(
+            [=](int v) {
+                const float d = pr[v] - qr[v];
+                return d > 0.f ? d : 0.f;
+            },
+            V, u, cp, &s_res);
+        if (rep < 0) rep = block_inv_cdf([=](int v) { return pr[v]; }, V, u, cp, &s_res);
+    }
+    for (int j = t; j < W; j += 256) {
+        const size_t row = (size_t)b * W + j;
+        int tok = -1;
+        if (j < count) tok = (j == count - 1 && rejected) ? rep : drafts[row];
+        tokens[row] = tok;
+    }
+    if (t == 0) counts[b] = count;
+}
+
+void verify_probs(int B, int W, int V, const float* p, const float* q, const int32_t* drafts,
+                  const float* u_acc, const float* u_res, int32_t* counts, int32_t* tokens,
+                  hipStream_t s) {
+    if (B <= 0) return;
+    hipLaunchKernelGGL(k_verify_probs, dim3(B), dim3(256), 0, s, W, V, p, q, drafts, u_acc, u_res,
+                       counts, tokens);
+}
+
+}  // namespace hbsjd
