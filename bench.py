@@ -1,0 +1,273 @@
+"""Benchmark of the batched SJD rollout on one MI355X.
+
+A step is one whole rollout (prefill, first window, then verification rounds
+until every image holds T tokens) of the LlamaGen-B-shaped workload: 12 layers,
+d 768, 12 heads, MLP 2048, vocab 16384, 16x16 grid, batch 32 with prefixes of
+uniform length 0-128, W = 16, H = 24, temperature 1.0, top-k 2000, bf16,
+seeded random-init weights and synthetic prefixes. Inputs are resident on the
+GPU before timing starts. Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "committed tokens/s per MI355X for batched SJD rollout; mean accepted tokens/round"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+GEMMS = {  # class: (N, K, output bytes per output column and row)
+    "qkv": lambda d, f, V, e: (3 * d, d, e),        # q, K, V written in the compute dtype
+    "oproj": lambda d, f, V, e: (d, d, 8),          # fp32 residual read and written
+    "w13": lambda d, f, V, e: (2 * f, d, e / 2),    # SwiGLU writes f of the 2f columns
+    "w2": lambda d, f, V, e: (d, f, 8),
+    "lmhead": lambda d, f, V, e: (V, d, 4),         # fp32 logits
+}
+
+
+def launch_work(cls, shape, rows, keys=0, seq_keys=0, esz=2):
+    """Algorithmic (bytes, flops) of ONE launch of a kernel class over `rows`
+    rows of active images. GEMMs read the weights once and the activations once;
+    attention reads each sequence's K and V once (seq_keys = sum over sequences
+    of keys read) and does 4 d flops per (row, key) pair (keys = sum over rows of
+    keys attended); the transform reads a logits row and writes a probability row."""
+    d, f, V = shape.d_model, shape.mlp_hidden, shape.vocab
+    if cls in GEMMS:
+        N, K, ob = GEMMS[cls](d, f, V, esz)
+        return N * K * esz + rows * K * esz + rows * N * ob, 2.0 * rows * N * K
+    if cls == "attn":
+        return seq_keys * 2 * d * esz + rows * 2 * d * esz, 4.0 * d * keys
+    if cls == "transform":
+        return rows * V * 8.0, 0.0
+    if cls == "norm":
+        return rows * d * (4.0 + esz), 0.0
+    return 0.0, 0.0
+
+
+def rollout_work(cls, shape, prefix_len, counts, W, cfg, esz=2):
+    """Algorithmic (bytes, flops) of every launch of `cls` in one rollout, from the
+    per-round commit counts (host array [rounds, B]); only active images count."""
+    T, L = shape.T, shape.n_layers
+    k = prefix_len.astype(np.int64)
+    act = k < T
+    ka = k[act]
+    tot_b = tot_f = 0.0
+
+    def add(n_launch, rows, keys=0, seq_keys=0):
+        nonlocal tot_b, tot_f
+        b, fl = launch_work(cls, shape, rows, keys, seq_keys, esz)
+        tot_b += n_launch * b
+        tot_f += n_launch * fl
+
+    pf_rows = int(np.sum(ka + 1)) * cfg
+    n_seq = int(act.sum()) * cfg
+    pf_keys = int(np.sum((ka + 1) * (ka + 2) // 2)) * cfg
+    if cls in ("qkv", "oproj", "w13", "w2"):
+        add(L, pf_rows)
+    elif cls == "attn":
+        add(L, pf_rows, pf_keys, pf_rows)
+    elif cls == "norm":
+        add(2 * L - 1, pf_rows)
+        add(1, n_seq)
+    elif cls == "lmhead":
+        add(1, n_seq)
+    elif cls == "transform":
+        add(1, int(act.sum()))
+    cur = k.copy()
+    for r in range(counts.shape[0]):
+        a = cur < T
+        A = int(a.sum())
+        if A == 0:
+            break
+        rows = A * cfg * (W + 1)
+        n = cur[a]
+        keys = int(np.sum((W + 1) * (n + 1) + W * (W + 1) // 2)) * cfg
+        seq_keys = int(np.sum(n + W + 1)) * cfg
+        if cls in ("qkv", "oproj", "w13", "w2"):
+            add(L, rows)
+        elif cls == "attn":
+            add(L, rows, keys, seq_keys)
+        elif cls == "norm":
+            add(2 * L, rows)
+        elif cls == "lmhead":
+            add(1, rows)
+        elif cls == "transform":
+            add(1, A * (W + 1))
+        cur = cur + counts[r]
+    return tot_b, tot_f
+
+
+def cpu_baseline(shape, blob_rounded, batch, wl, n_img, rounds):
+    """The oracle on the host: the first n_img images of the same batch, prefill
+    plus `rounds` verification rounds; committed tokens per second."""
+    import oracle
+    import synth
+    om = oracle.Model(shape, blob_rounded)
+    sub = synth.Batch(batch.prefix_tokens[:n_img].copy(), batch.prefix_len[:n_img].copy(),
+                      batch.labels[:n_img].copy(), batch.temperature[:n_img].copy())
+    t0 = time.perf_counter()
+    r = om.rollout(sub, W=wl.window, H=wl.history, top_k=wl.top_k, cfg_scale=wl.cfg_scale,
+                   seed=1000, exec_mode=1, max_rounds=rounds, allow_partial=True)
+    dt = time.perf_counter() - t0
+    committed = int(r["counts"].sum())
+    return committed / dt, committed, dt
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="llamagen_b")
+    ap.add_argument("--exec-mode", default="auto", choices=["auto", "full", "compact"])
+    ap.add_argument("--gamma", type=int, default=-1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=0, help="images in the CPU sample (0 = auto)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the rollout shards by image with no "
+              f"cross-GPU exchange, and this build measures the single-GPU path "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2608_18183_amd as P
+    import synth
+
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    shape = wl.model
+    T = shape.T
+    blob = synth.make_weights(shape, 0, std=wl.weight_std, bias_std=wl.bias_std)
+    batch = synth.make_batch(wl, 1)
+    B = wl.batch
+    cfg = 2 if wl.cfg_scale else 1
+    desc = P.ModelDesc(shape.n_layers, shape.d_model, shape.n_heads, shape.mlp_hidden,
+                       shape.vocab, shape.n_classes, shape.grid,
+                       P.DTYPE_BF16 if wl.dtype == "bf16" else P.DTYPE_F32,
+                       bool(shape.has_lm_bias), shape.rms_eps, shape.rope_base)
+    ctx = P.Context(desc)
+    ctx.hbsjd_load_weights(blob)
+    prefix = torch.from_numpy(batch.prefix_tokens).cuda()
+    max_rounds = int(T - batch.prefix_len.min())
+    out_tokens = torch.empty((B, T), dtype=torch.int32, device="cuda")
+    out_counts = torch.empty((max_rounds, B), dtype=torch.int32, device="cuda")
+    mode = {"auto": P.EXEC_AUTO, "full": P.EXEC_FULL, "compact": P.EXEC_COMPACT}[args.exec_mode]
+
+    def step(seed):
+        return ctx.hbsjd_rollout(prefix, batch.prefix_len, batch.labels, batch.temperature,
+                                 wl.window, history=wl.history, top_k=wl.top_k,
+                                 cfg_scale=wl.cfg_scale, seed=seed, exec_mode=mode,
+                                 gamma=args.gamma, max_rounds=max_rounds, out_tokens=out_tokens,
+                                 out_counts=out_counts)
+
+    # warm-up; the first warm-up rollout also times every kernel class to find
+    # the dominant one
+    dominant = None
+    for i in range(max(args.warmup, 1)):
+        if i == 0:
+            ctx.hbsjd_profile_start(P.KERNELS)
+        step(999 - i)
+        if i == 0:
+            prof = ctx.hbsjd_profile_read()
+            ctx.hbsjd_profile_start(())
+            dominant = max(prof, key=lambda k: prof[k][0])
+    torch.cuda.synchronize()
+    # timed region: only the dominant class is bracketed by events
+    ctx.hbsjd_profile_start([dominant])
+    results = []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        results.append(step(1000 + i))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom_ms, dom_n = ctx.hbsjd_profile_read()[dominant]
+    ctx.hbsjd_profile_start(())
+
+    committed_per_step = int(np.sum(T - batch.prefix_len))
+    value = committed_per_step * args.steps / elapsed
+    counts_total = sum(int(r["verified"]) for r in results)    # committed tokens = sum of counts
+    image_rounds = sum(r["image_rounds"] for r in results)
+    rounds = [r["rounds"] for r in results]
+    mean_accepted = counts_total / max(image_rounds, 1)
+    reject_rate = sum(r["rejected"] for r in results) / max(counts_total, 1)
+
+    # roofline of the dominant kernel class over the timed region
+    tb = tf = 0.0
+    for r in results:
+        b, fl = rollout_work(dominant, shape, batch.prefix_len, r["counts"].cpu().numpy(),
+                             wl.window, cfg, esz=2 if wl.dtype == "bf16" else 4)
+        tb += b
+        tf += fl
+    t_s = dom_ms / 1e3
+    hbm_t, mfma_t = tb / (HBM_PEAK_GBS * 1e9), tf / (BF16_PEAK_TFLOPS * 1e12)
+    if mfma_t > hbm_t:
+        roof = {"bound": "mfma", "achieved": round(tf / t_s / 1e12, 3), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(tb / t_s / 1e9, 2), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
+    roof["traffic"] = None
+    roof["kernel"] = dominant
+    roof["launches"] = dom_n
+    roof["avg_launch_us"] = round(1000.0 * dom_ms / max(dom_n, 1), 3)
+    roof["time_share"] = round(t_s / elapsed, 4)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from tests.gpu_util import bf16_rounded_blob
+        cores = min(16, os.cpu_count() or 1)
+        n_img = args.cpu_images or min(cores, B)
+        rb = bf16_rounded_blob(shape, blob) if wl.dtype == "bf16" else blob
+        v, committed, dt = cpu_baseline(shape, rb, batch, wl, n_img, rounds=6)
+        cpu = {"value": round(v, 2), "unit": "tokens/s", "cores": min(cores, n_img),
+               "kind": "oracle",
+               "sample": f"first {n_img} images of the same batch, prefill + 6 rounds "
+                         f"({committed} committed tokens in {dt:.1f} s), fp32 oracle on the "
+                         f"bf16-rounded weights"}
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1000.0 * elapsed / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights, uniform random prefixes)",
+        "config": {"workload": f"{args.workload}: {shape.n_layers}L d{shape.d_model} "
+                               f"h{shape.n_heads} f{shape.mlp_hidden} V{shape.vocab} "
+                               f"{shape.grid}x{shape.grid}, batch {B}, W {wl.window}, "
+                               f"top-k {wl.top_k}, cfg {wl.cfg_scale}",
+                   "batch": B, "window": wl.window, "history": wl.history,
+                   "exec_mode": args.exec_mode, "parallelism": "single GPU"},
+        "mean_accepted_tokens_per_round": round(mean_accepted, 4),
+        "rounds_per_step": rounds,
+        "reject_rate": round(reject_rate, 4),
+        "committed_tokens_per_step": committed_per_step,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -217,6 +217,40 @@ hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t
 hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* ctx, int32_t batch, int32_t window,
                                    int32_t* gamma);
 
+/*
+ * Per-kernel timing on the context's stream, for measurement. Kernel classes
+ * of one verifier round (and of the prefill, which runs the same kernels).
+ */
+typedef enum hbsjd_kernel {
+    HBSJD_K_SETUP = 0,      /* active compaction, mode choice, row assembly */
+    HBSJD_K_EMBED = 1,      /* embedding gather + first RMSNorm */
+    HBSJD_K_QKV = 2,        /* QKV GEMM + 2D RoPE + paged KV append */
+    HBSJD_K_ATTN = 3,       /* causal attention over the paged cache */
+    HBSJD_K_OPROJ = 4,      /* O projection + residual */
+    HBSJD_K_NORM = 5,       /* RMSNorm (mid-layer, next layer, final) */
+    HBSJD_K_W13 = 6,        /* W1|W3 GEMM + SwiGLU */
+    HBSJD_K_W2 = 7,         /* W2 GEMM + residual */
+    HBSJD_K_LMHEAD = 8,     /* lm_head GEMM (+ bias) */
+    HBSJD_K_TRANSFORM = 9,  /* CFG, temperature, top-k, softmax, chunk prefix */
+    HBSJD_K_VERIFY = 10,    /* verification, commit, window refresh */
+    HBSJD_K_COUNT = 11
+} hbsjd_kernel;
+
+/*
+ * Start timing: from now on every launch of the classes whose bit is set in
+ * `class_mask` (bit k = hbsjd_kernel k) is bracketed by HIP events on the
+ * context's stream; counters restart at zero. class_mask 0 stops timing.
+ * Timing adds an event record per launch and does not change results.
+ */
+hbsjd_status hbsjd_profile_start(hbsjd_ctx* ctx, uint32_t class_mask);
+
+/*
+ * Read the accumulated timing (synchronises the stream): host arrays of
+ * HBSJD_K_COUNT entries, total milliseconds and launch counts per class; either
+ * may be NULL.
+ */
+hbsjd_status hbsjd_profile_read(hbsjd_ctx* ctx, double* total_ms, int64_t* launches);
+
 /* Release the context and its device memory (NULL is ignored). */
 void hbsjd_destroy(hbsjd_ctx* ctx);
 

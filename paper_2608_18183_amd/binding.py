@@ -20,6 +20,8 @@ _lib = None
 DTYPE_F32, DTYPE_BF16 = 0, 1
 EXEC_AUTO, EXEC_FULL, EXEC_COMPACT = 0, 1, 2
 VERIFY_PROB, VERIFY_GREEDY = 0, 1
+KERNELS = ["setup", "embed", "qkv", "attn", "oproj", "norm", "w13", "w2", "lmhead",
+           "transform", "verify"]
 _STATUS = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EHIP", 4: "ESTATE", 5: "EINTERNAL"}
 
 _P = ctypes.c_void_p
@@ -62,6 +64,8 @@ _SIGS = {
     "hbsjd_verify_probs": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
+    "hbsjd_profile_start": (_I32, [_P, ctypes.c_uint32]),
+    "hbsjd_profile_read": (_I32, [_P, _P, _P]),
     "hbsjd_destroy": (None, [_P]),
     "hbsjd_last_error": (ctypes.c_char_p, []),
     "hbsjd_version": (ctypes.c_char_p, []),
@@ -252,6 +256,18 @@ class Context:
         _check(self._lib.hbsjd_forward(self._h, ln.size, _P(_dev_ptr(tokens)), _np_ptr(ln),
                                        _np_ptr(lab), _P(_dev_ptr(out))), "hbsjd_forward")
         return out
+
+    def hbsjd_profile_start(self, classes=()):
+        mask = 0
+        for k in classes:
+            mask |= 1 << KERNELS.index(k)
+        _check(self._lib.hbsjd_profile_start(self._h, mask), "hbsjd_profile_start")
+
+    def hbsjd_profile_read(self) -> dict:
+        ms = np.zeros(len(KERNELS), dtype=np.float64)
+        n = np.zeros(len(KERNELS), dtype=np.int64)
+        _check(self._lib.hbsjd_profile_read(self._h, _np_ptr(ms), _np_ptr(n)), "hbsjd_profile_read")
+        return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNELS)}
 
     def hbsjd_calibrate_gamma(self, batch: int, window: int) -> int:
         g = np.zeros(1, dtype=np.int32)

@@ -22,6 +22,13 @@
 
 using namespace hbsjd;
 
+namespace hbsjd {
+LaunchEvents* launch_events() {
+    static thread_local LaunchEvents slot;
+    return &slot;
+}
+}  // namespace hbsjd
+
 namespace {
 
 thread_local std::string g_err;
@@ -79,6 +86,13 @@ struct hbsjd_ctx {
     uint64_t seed = 0;
     int32_t* counts = nullptr;   // device [max_rounds][B]
     long kv_layer_elems = 0;
+
+    // per-kernel-class timing (hbsjd_profile_start / hbsjd_profile_read)
+    uint32_t prof_mask = 0;
+    std::vector<hipEvent_t> prof_free;
+    std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> prof_pending;
+    double prof_ms[HBSJD_K_COUNT] = {};
+    int64_t prof_n[HBSJD_K_COUNT] = {};
 
     ~hbsjd_ctx();
 };
@@ -143,9 +157,72 @@ hbsjd_ctx::~hbsjd_ctx() {
     if (pin) (void)hipHostFree(pin);
     for (auto& e : ev)
         if (e) (void)hipEventDestroy(e);
+    for (auto& pr : prof_pending) {
+        (void)hipEventDestroy(pr.second.first);
+        (void)hipEventDestroy(pr.second.second);
+    }
+    for (hipEvent_t e : prof_free) (void)hipEventDestroy(e);
 }
 
 namespace {
+
+// ---------------------------------------------------------------- timing
+
+hipEvent_t prof_event(hbsjd_ctx* c) {
+    if (!c->prof_free.empty()) {
+        hipEvent_t e = c->prof_free.back();
+        c->prof_free.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    (void)hipEventCreate(&e);
+    return e;
+}
+
+// fold finished event pairs into the per-class totals
+void prof_resolve(hbsjd_ctx* c) {
+    if (c->prof_pending.empty()) return;
+    (void)hipEventSynchronize(c->prof_pending.back().second.second);
+    for (auto& pr : c->prof_pending) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, pr.second.first, pr.second.second) == hipSuccess) {
+            c->prof_ms[pr.first] += ms;
+            c->prof_n[pr.first] += 1;
+        }
+        c->prof_free.push_back(pr.second.first);
+        c->prof_free.push_back(pr.second.second);
+    }
+    c->prof_pending.clear();
+}
+
+// arms the launch-event slot for the one kernel launched inside this scope
+// when its class is timed
+struct Timed {
+    hbsjd_ctx* c;
+    int cls;
+    bool armed = false;
+    Timed(hbsjd_ctx* ctx, int k) : c(ctx), cls(k) {
+        if (c->prof_mask & (1u << k)) {
+            LaunchEvents* ev = launch_events();
+            ev->start = prof_event(c);
+            ev->stop = prof_event(c);
+            ev->used = false;
+            armed = true;
+        }
+    }
+    ~Timed() {
+        if (!armed) return;
+        LaunchEvents* ev = launch_events();
+        if (ev->used) {
+            c->prof_pending.push_back({cls, {ev->start, ev->stop}});
+        } else {   // nothing was launched (empty row range)
+            c->prof_free.push_back(ev->start);
+            c->prof_free.push_back(ev->stop);
+        }
+        *ev = LaunchEvents{};
+        if (c->prof_pending.size() >= 8192) prof_resolve(c);
+    }
+};
 
 // ---------------------------------------------------------------- validation
 
@@ -201,24 +278,49 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
     const bool bf = c->bf16;
     hipStream_t s = c->stream;
     const int d = c->d, f = c->f;
-    embed_norm(bf, r.meta, r.nrows_dev, r.nrows_cap, c->tok_emb, c->cls_emb, c->g_attn[0],
-               c->m.rms_eps, d, as<float>(c->h), c->hb.p, s);
+    {
+        Timed tm(c, HBSJD_K_EMBED);
+        embed_norm(bf, r.meta, r.nrows_dev, r.nrows_cap, c->tok_emb, c->cls_emb, c->g_attn[0],
+                   c->m.rms_eps, d, as<float>(c->h), c->hb.p, s);
+    }
     const float* rc = as<float>(c->rope);
     const float* rs = rc + (size_t)(c->T + 1) * (c->dh / 2);
     for (int l = 0; l < c->L; ++l) {
         QkvArgs qa{c->qb.p, kv_layer(c, l), r.meta.pos, r.meta.kv, rc, rs, d, c->H, c->dh, c->T};
-        gemm_qkv(bf, c->hb.p, d, c->wqkv[l], 3 * d, d, r.nrows_dev, r.nrows_cap, qa, s);
-        attention(bf, c->qb.p, c->ob.p, d, c->H, c->dh, kv_layer(c, l), as<int32_t>(c->ptab),
-                  c->max_pages, r.seg, r.nseg_dev, r.nseg_cap, r.max_rows_per_seg, r.meta,
-                  r.nrows_dev, r.nrows_cap, s);
-        gemm_residual(bf, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap, as<float>(c->h), s);
-        rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_ffn[l], c->m.rms_eps,
-                d, c->hb.p, s);
-        gemm_swiglu(bf, c->hb.p, d, c->w13[l], 2 * f, d, r.nrows_dev, r.nrows_cap, c->act.p, s);
-        gemm_residual(bf, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap, as<float>(c->h), s);
-        if (l + 1 < c->L)
+        {
+            Timed tm(c, HBSJD_K_QKV);
+            gemm_qkv(bf, c->hb.p, d, c->wqkv[l], 3 * d, d, r.nrows_dev, r.nrows_cap, qa, s);
+        }
+        {
+            Timed tm(c, HBSJD_K_ATTN);
+            attention(bf, c->qb.p, c->ob.p, d, c->H, c->dh, kv_layer(c, l), as<int32_t>(c->ptab),
+                      c->max_pages, r.seg, r.nseg_dev, r.nseg_cap, r.max_rows_per_seg, r.meta,
+                      r.nrows_dev, r.nrows_cap, s);
+        }
+        {
+            Timed tm(c, HBSJD_K_OPROJ);
+            gemm_residual(bf, 0, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap,
+                          as<float>(c->h), s);
+        }
+        {
+            Timed tm(c, HBSJD_K_NORM);
+            rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_ffn[l],
+                    c->m.rms_eps, d, c->hb.p, s);
+        }
+        {
+            Timed tm(c, HBSJD_K_W13);
+            gemm_swiglu(bf, c->hb.p, d, c->w13[l], 2 * f, d, r.nrows_dev, r.nrows_cap, c->act.p, s);
+        }
+        {
+            Timed tm(c, HBSJD_K_W2);
+            gemm_residual(bf, 1, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap,
+                          as<float>(c->h), s);
+        }
+        if (l + 1 < c->L) {
+            Timed tm(c, HBSJD_K_NORM);
             rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_attn[l + 1],
                     c->m.rms_eps, d, c->hb.p, s);
+        }
     }
 }
 
@@ -492,7 +594,10 @@ hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
                       as<int32_t>(c->row_kv), as<int32_t>(c->row_seq), as<int32_t>(c->seg_seq),
                       as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0),
                       mt, as<int32_t>(c->a_hist), as<int32_t>(c->mode_hist)};
-    round_setup(sa, s);
+    {
+        Timed tm(c, HBSJD_K_SETUP);
+        round_setup(sa, s);
+    }
     const int rows_cap = S * R;
     FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
                        as<int32_t>(c->row_seq)},
@@ -501,20 +606,33 @@ hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
                         as<int32_t>(c->seg_pos0)},
                mt + kMetaSegs, S, R};
     forward_layers(c, fr);
-    rmsnorm(c->bf16, as<float>(c->h), nullptr, mt + kMetaRows, rows_cap, c->g_out, c->m.rms_eps,
-            c->d, c->hb.p, s);
+    {
+        Timed tm(c, HBSJD_K_NORM);
+        rmsnorm(c->bf16, as<float>(c->h), nullptr, mt + kMetaRows, rows_cap, c->g_out,
+                c->m.rms_eps, c->d, c->hb.p, s);
+    }
     float* lg = cfg == 1 ? as<float>(c->P[cur]) : as<float>(c->logits);
-    gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg, c->b_lm, s);
+    {
+        Timed tm(c, HBSJD_K_LMHEAD);
+        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg,
+                    c->b_lm, s);
+    }
     TransformArgs ta{lg, as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
                      as<int32_t>(c->slot_img), as<float>(c->temps), R, cfg, c->V, c->top_k,
                      c->cfg_scale, mt + kMetaOutRows, B * R, mt};
-    transform(ta, s);
+    {
+        Timed tm(c, HBSJD_K_TRANSFORM);
+        transform(ta, s);
+    }
     VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds, c->seed,
                   as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
                   as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
                   as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt};
-    verify_commit(va, s);
+    {
+        Timed tm(c, HBSJD_K_VERIFY);
+        verify_commit(va, s);
+    }
     HIPTRY(c, hipGetLastError());
     c->rounds_launched = r + 1;
     return HBSJD_OK;
@@ -928,6 +1046,36 @@ hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t
         return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_philox");
+    }
+}
+
+hbsjd_status hbsjd_profile_start(hbsjd_ctx* c, uint32_t class_mask) {
+    try {
+        GUARD(c);
+        prof_resolve(c);
+        for (int k = 0; k < HBSJD_K_COUNT; ++k) {
+            c->prof_ms[k] = 0.0;
+            c->prof_n[k] = 0;
+        }
+        c->prof_mask = class_mask & ((1u << HBSJD_K_COUNT) - 1);
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_profile_start");
+    }
+}
+
+hbsjd_status hbsjd_profile_read(hbsjd_ctx* c, double* total_ms, int64_t* launches) {
+    try {
+        GUARD(c);
+        HIPTRY(c, hipStreamSynchronize(c->stream));
+        prof_resolve(c);
+        for (int k = 0; k < HBSJD_K_COUNT; ++k) {
+            if (total_ms) total_ms[k] = c->prof_ms[k];
+            if (launches) launches[k] = c->prof_n[k];
+        }
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_profile_read");
     }
 }
 

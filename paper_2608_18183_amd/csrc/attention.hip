@@ -261,27 +261,27 @@ void attention(bool bf16, const void* q, void* o, int d, int heads, int head_dim
     if (bf16) {
         if (nseg_cap <= 0) return;
         if (max_rows_per_seg <= 16) {
-            hipLaunchKernelGGL(k_attn_bf16<1>, dim3(nseg_cap, heads), dim3(256), 0, s,
+            launch(k_attn_bf16<1>, dim3(nseg_cap, heads), dim3(256), 0, s,
                                (const uint16_t*)q, (uint16_t*)o, d, heads,
                                (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
         } else if (max_rows_per_seg <= 32) {
-            hipLaunchKernelGGL(k_attn_bf16<2>, dim3(nseg_cap, heads), dim3(256), 0, s,
+            launch(k_attn_bf16<2>, dim3(nseg_cap, heads), dim3(256), 0, s,
                                (const uint16_t*)q, (uint16_t*)o, d, heads,
                                (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
         } else if (max_rows_per_seg <= 48) {
-            hipLaunchKernelGGL(k_attn_bf16<3>, dim3(nseg_cap, heads), dim3(256), 0, s,
+            launch(k_attn_bf16<3>, dim3(nseg_cap, heads), dim3(256), 0, s,
                                (const uint16_t*)q, (uint16_t*)o, d, heads,
                                (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
         } else {
             const int qblocks = (max_rows_per_seg + 63) / 64;
-            hipLaunchKernelGGL(k_attn_bf16<4>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
+            launch(k_attn_bf16<4>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
                                (const uint16_t*)q, (uint16_t*)o, d, heads,
                                (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev,
                                qblocks);
         }
     } else {
         if (nrows_cap <= 0) return;
-        hipLaunchKernelGGL(k_attn_f32, dim3(nrows_cap, heads), dim3(64), 0, s, (const float*)q,
+        launch(k_attn_f32, dim3(nrows_cap, heads), dim3(64), 0, s, (const float*)q,
                            (float*)o, d, heads, head_dim, (const float*)kv_layer, ptab, max_pages,
                            rows, nrows_dev);
     }

@@ -56,6 +56,7 @@ struct EpiQkv {
     }
 };
 
+template <int Tag>   // 0 after the O projection, 1 after W2 (distinct kernel names)
 struct EpiResidual {
     float* h;
     int ld;
@@ -205,7 +206,7 @@ static void launch_bf16(const void* A, int lda, const void* W, int N, int K, con
     if (m_cap <= 0) return;
     const int tiles = ((m_cap + BM - 1) / BM) * (N / BN);
     const int grid = ((tiles + 7) / 8) * 8;
-    hipLaunchKernelGGL((k_gemm_bf16<BM, BN, Epi>), dim3(grid), dim3(256), 0, s,
+    launch(k_gemm_bf16<BM, BN, Epi>, dim3(grid), dim3(256), 0, s,
                        (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, epi);
 }
 
@@ -278,7 +279,7 @@ static void launch_f32(const void* A, int lda, const void* W, int N, int K, cons
                        int m_cap, const Epi& epi, hipStream_t s) {
     if (m_cap <= 0) return;
     dim3 grid((N + 63) / 64, (m_cap + 63) / 64);
-    hipLaunchKernelGGL((k_gemm_f32<Epi>), grid, dim3(256), 0, s, (const float*)A, lda,
+    launch(k_gemm_f32<Epi>, grid, dim3(256), 0, s, (const float*)A, lda,
                        (const float*)W, N, K, m_dev, m_cap, epi);
 }
 
@@ -297,13 +298,22 @@ void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, co
     }
 }
 
-void gemm_residual(bool bf16, const void* A, int lda, const void* W, int N, int K,
-                   const int* m_dev, int m_cap, float* h, hipStream_t s) {
-    EpiResidual epi{h, N};
+template <int Tag>
+static void residual_tag(bool bf16, const void* A, int lda, const void* W, int N, int K,
+                         const int* m_dev, int m_cap, float* h, hipStream_t s) {
+    EpiResidual<Tag> epi{h, N};
     if (bf16)
         dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, epi, s);
     else
         launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
+}
+
+void gemm_residual(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
+                   const int* m_dev, int m_cap, float* h, hipStream_t s) {
+    if (tag == 0)
+        residual_tag<0>(bf16, A, lda, W, N, K, m_dev, m_cap, h, s);
+    else
+        residual_tag<1>(bf16, A, lda, W, N, K, m_dev, m_cap, h, s);
 }
 
 void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,

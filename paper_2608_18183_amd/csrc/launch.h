@@ -1,11 +1,33 @@
 // Host-side launchers of the library's kernels (internal interface).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 namespace hbsjd {
+
+// Optional kernel timing: when a caller arms the per-thread slot, the next
+// launch through launch() carries the start/stop events in its own dispatch
+// (hipExtLaunchKernelGGL), so they time the kernel itself.
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+    bool used = false;
+};
+LaunchEvents* launch_events();
+
+template <typename K, typename... Args>
+inline void launch(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+    LaunchEvents* ev = launch_events();
+    if (ev->start && !ev->used) {
+        ev->used = true;
+        hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev->start, ev->stop, 0u, args...);
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+    }
+}
 
 // The paged KV cache of one layer is an array of pages of 64 slots; page p
 // holds, for every head h, K as [64 slots][head_dim] at
@@ -45,7 +67,7 @@ struct QkvArgs {
 
 void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
               int m_cap, const QkvArgs& e, hipStream_t s);
-void gemm_residual(bool bf16, const void* A, int lda, const void* W, int N, int K,
+void gemm_residual(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
                    const int* m_dev, int m_cap, float* h, hipStream_t s);
 void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s);

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
 }
 
 void round_setup(const RoundSetupArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(k_round_setup, dim3(1), dim3(1024), 0, s, a);
+    launch(k_round_setup, dim3(1), dim3(1024), 0, s, a);
 }
 
 // ---------------------------------------------------------------- prefill rows
@@ -128,7 +128,7 @@ __global__ void k_prefill_rows(PrefillRowsArgs a) {
 
 void prefill_rows(const PrefillRowsArgs& a, hipStream_t s) {
     if (a.total_rows <= 0) return;
-    hipLaunchKernelGGL(k_prefill_rows, dim3((a.total_rows + 255) / 256), dim3(256), 0, s, a);
+    launch(k_prefill_rows, dim3((a.total_rows + 255) / 256), dim3(256), 0, s, a);
 }
 
 __global__ void k_check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V,
@@ -146,7 +146,7 @@ void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V
                   hipStream_t s) {
     const int n = B * T;
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_check_prefix, dim3((n + 255) / 256), dim3(256), 0, s, prefix, len, B, T,
+    launch(k_check_prefix, dim3((n + 255) / 256), dim3(256), 0, s, prefix, len, B, T,
                        V, err);
 }
 
@@ -184,11 +184,11 @@ void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_
                 float* h, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     if (bf16)
-        hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, rows,
+        launch(k_embed_norm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, rows,
                            nrows_dev, (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain,
                            eps, d, h, (uint16_t*)hb);
     else
-        hipLaunchKernelGGL(k_embed_norm<float>, dim3(nrows_cap), dim3(256), 0, s, rows, nrows_dev,
+        launch(k_embed_norm<float>, dim3(nrows_cap), dim3(256), 0, s, rows, nrows_dev,
                            (const float*)tok_emb, (const float*)cls_emb, gain, eps, d, h,
                            (float*)hb);
 }
@@ -208,10 +208,10 @@ void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     if (bf16)
-        hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
+        launch(k_rmsnorm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
                            nrows_dev, gain, eps, d, (uint16_t*)hb);
     else
-        hipLaunchKernelGGL(k_rmsnorm<float>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
+        launch(k_rmsnorm<float>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
                            nrows_dev, gain, eps, d, (float*)hb);
 }
 
@@ -228,7 +228,7 @@ __global__ void k_philox(uint64_t seed, int n, const uint32_t* bt, uint32_t* out
 
 void philox_fill(uint64_t seed, int n, const uint32_t* bt, uint32_t* out, hipStream_t s) {
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_philox, dim3((n + 255) / 256), dim3(256), 0, s, seed, n, bt, out);
+    launch(k_philox, dim3((n + 255) / 256), dim3(256), 0, s, seed, n, bt, out);
 }
 
 }  // namespace hbsjd

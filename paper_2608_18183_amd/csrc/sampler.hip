@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
 
 void transform(const TransformArgs& a, hipStream_t s) {
     if (a.nout_cap <= 0) return;
-    hipLaunchKernelGGL(k_transform, dim3(a.nout_cap), dim3(256), 0, s, a);
+    launch(k_transform, dim3(a.nout_cap), dim3(256), 0, s, a);
 }
 
 // ---------------------------------------------------------------- inverse CDF helpers
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
 
 void verify_commit(const VerifyArgs& a, hipStream_t s) {
     if (a.nimg_cap <= 0) return;
-    hipLaunchKernelGGL(k_verify, dim3(a.nimg_cap), dim3(256), 0, s, a);
+    launch(k_verify, dim3(a.nimg_cap), dim3(256), 0, s, a);
 }
 
 // ---------------------------------------------------------------- explicit-row verification
@@ -553,7 +553,7 @@ void verify_probs(int B, int W, int V, const float* p, const float* q, const int
                   const float* u_acc, const float* u_res, int32_t* counts, int32_t* tokens,
                   hipStream_t s) {
     if (B <= 0) return;
-    hipLaunchKernelGGL(k_verify_probs, dim3(B), dim3(256), 0, s, W, V, p, q, drafts, u_acc, u_res,
+    launch(k_verify_probs, dim3(B), dim3(256), 0, s, W, V, p, q, drafts, u_acc, u_res,
                        counts, tokens);
 }
 
