@@ -28,9 +28,9 @@ BF16_PEAK_TFLOPS = 2500.0
 
 GEMMS = {  # class: (N, K, output bytes per output column and row)
     "qkv": lambda d, f, V, e: (3 * d, d, e),        # q, K, V written in the compute dtype
-    "oproj": lambda d, f, V, e: (d, d, 8),          # fp32 residual read and written
+    "oproj": lambda d, f, V, e: (d, d, 4),          # fp32 partial sums written
     "w13": lambda d, f, V, e: (2 * f, d, e / 2),    # SwiGLU writes f of the 2f columns
-    "w2": lambda d, f, V, e: (d, f, 8),
+    "w2": lambda d, f, V, e: (d, f, 4),
     "lmhead": lambda d, f, V, e: (V, d, 4),         # fp32 logits
 }
 
@@ -49,8 +49,8 @@ def launch_work(cls, shape, rows, keys=0, seq_keys=0, esz=2):
         return seq_keys * 2 * d * esz + rows * 2 * d * esz, 4.0 * d * keys
     if cls == "transform":
         return rows * V * 8.0, 0.0
-    if cls == "norm":
-        return rows * d * (4.0 + esz), 0.0
+    if cls == "norm":     # partial sums read, residual read and written, normed row written
+        return rows * d * (4.0 + 8.0 + esz), 0.0
     return 0.0, 0.0
 
 

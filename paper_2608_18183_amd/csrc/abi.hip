@@ -16,6 +16,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -50,7 +51,9 @@ struct hbsjd_ctx {
     int L = 0, d = 0, H = 0, dh = 0, f = 0, V = 0, C = 0, G = 0, T = 0, nC = 0;
     bool bf16 = false;
     size_t esz = 4;
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr;       // the library's own stream (default priority)
+    hipStream_t user_stream = nullptr;  // the caller's stream: work starts after its work
+    hipEvent_t ev_user = nullptr;
     int device = 0;
     uint64_t max_kv_bytes = 0;
     bool poisoned = false;
@@ -71,7 +74,7 @@ struct hbsjd_ctx {
     DevBuf row_tok, row_pos, row_kv, row_seq;
     DevBuf seg_seq, seg_row0, seg_nrows, seg_pos0;
     DevBuf slot_img, active_list, pf_slots;
-    DevBuf h, hb, qb, ob, act;
+    DevBuf h, hb, qb, ob, act, part;
     DevBuf P[2], CP[2], amax[2], logits;
     DevBuf seq_row0, seq_img, seq_branch, lm_idx;
     DevBuf ptab, kv;
@@ -86,6 +89,12 @@ struct hbsjd_ctx {
     uint64_t seed = 0;
     int32_t* counts = nullptr;   // device [max_rounds][B]
     long kv_layer_elems = 0;
+
+    // the round as two captured graphs (buffer parity 0 and 1), valid while the
+    // launch arguments they bake in stay the same
+    hipGraphExec_t gexec[2] = {nullptr, nullptr};
+    std::vector<uint64_t> gsig;
+    bool use_graphs = true;
 
     // per-kernel-class timing (hbsjd_profile_start / hbsjd_profile_read)
     uint32_t prof_mask = 0;
@@ -150,7 +159,7 @@ hbsjd_ctx::~hbsjd_ctx() {
     DevBuf* all[] = {&wbuf, &rope, &xtok, &cursor, &drafts, &qsrc, &labels, &temps, &plen,
                      &meta, &meta_pf, &a_hist, &mode_hist, &stats, &counts_own, &row_tok,
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
-                     &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &P[0], &P[1],
+                     &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
                      &CP[0], &CP[1], &amax[0], &amax[1], &logits, &seq_row0, &seq_img,
                      &seq_branch, &lm_idx, &ptab, &kv};
     for (DevBuf* b : all) free_buf(*b);
@@ -162,6 +171,10 @@ hbsjd_ctx::~hbsjd_ctx() {
         (void)hipEventDestroy(pr.second.second);
     }
     for (hipEvent_t e : prof_free) (void)hipEventDestroy(e);
+    for (auto& g : gexec)
+        if (g) (void)hipGraphExecDestroy(g);
+    if (ev_user) (void)hipEventDestroy(ev_user);
+    if (stream) (void)hipStreamDestroy(stream);
 }
 
 namespace {
@@ -248,6 +261,7 @@ std::string check_model(const hbsjd_model_desc& m) {
     if (!(m.rms_eps > 0.f) || !std::isfinite(m.rms_eps)) return "rms_eps must be positive";
     if (!(m.rope_base > 0.f) || !std::isfinite(m.rope_base)) return "rope_base must be positive";
     if ((long)m.grid * m.grid > 4096) return "grid too large";
+    if (m.d_model > 1536) return "d_model must be <= 1536";
     return "";
 }
 
@@ -273,7 +287,8 @@ void* kv_layer(hbsjd_ctx* c, int l) {
     return (char*)c->kv.p + (size_t)l * c->kv_layer_elems * c->esz;
 }
 
-// decoder layers; leaves the residual stream in h (the final norm is the caller's)
+// decoder layers; leaves the residual stream in h and its final RMSNorm (gain
+// g_out) in hb
 void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
     const bool bf = c->bf16;
     hipStream_t s = c->stream;
@@ -297,15 +312,18 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
                       c->max_pages, r.seg, r.nseg_dev, r.nseg_cap, r.max_rows_per_seg, r.meta,
                       r.nrows_dev, r.nrows_cap, s);
         }
+        // split-K applies to the MFMA path only; the fp32 path writes one partial
+        const int so = bf ? split_for(r.nrows_cap, d, d) : 1;
+        const int s2 = bf ? split_for(r.nrows_cap, d, f) : 1;
         {
             Timed tm(c, HBSJD_K_OPROJ);
-            gemm_residual(bf, 0, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap,
-                          as<float>(c->h), s);
+            gemm_partial(bf, 0, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap, so,
+                         as<float>(c->part), s);
         }
         {
             Timed tm(c, HBSJD_K_NORM);
-            rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_ffn[l],
-                    c->m.rms_eps, d, c->hb.p, s);
+            reduce_residual_norm(bf, as<float>(c->part), so, r.nrows_cap, as<float>(c->h),
+                                 r.nrows_dev, c->g_ffn[l], c->m.rms_eps, d, c->hb.p, s);
         }
         {
             Timed tm(c, HBSJD_K_W13);
@@ -313,13 +331,15 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         }
         {
             Timed tm(c, HBSJD_K_W2);
-            gemm_residual(bf, 1, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap,
-                          as<float>(c->h), s);
+            gemm_partial(bf, 1, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap, s2,
+                         as<float>(c->part), s);
         }
-        if (l + 1 < c->L) {
+        {
+            // the next layer's attention norm, or the final norm after the last layer
             Timed tm(c, HBSJD_K_NORM);
-            rmsnorm(bf, as<float>(c->h), nullptr, r.nrows_dev, r.nrows_cap, c->g_attn[l + 1],
-                    c->m.rms_eps, d, c->hb.p, s);
+            reduce_residual_norm(bf, as<float>(c->part), s2, r.nrows_cap, as<float>(c->h),
+                                 r.nrows_dev, l + 1 < c->L ? c->g_attn[l + 1] : c->g_out,
+                                 c->m.rms_eps, d, c->hb.p, s);
         }
     }
 }
@@ -336,6 +356,10 @@ hbsjd_status ensure_acts(hbsjd_ctx* c, long rows) {
     TRY(ensure(c, c->row_pos, rows * 4));
     TRY(ensure(c, c->row_kv, rows * 4));
     TRY(ensure(c, c->row_seq, rows * 4));
+    const long sp = c->bf16 ? std::max(split_for((int)rows, c->d, c->d),
+                                       split_for((int)rows, c->d, c->f))
+                            : 1;
+    TRY(ensure(c, c->part, (size_t)sp * rows * d * 4));
     return HBSJD_OK;
 }
 
@@ -428,6 +452,8 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     c->exec_mode = a->exec_mode;
     c->gamma = a->gamma >= 0 ? a->gamma : (c->gamma_cal >= 0 ? c->gamma_cal : B / 2);
     c->seed = a->seed;
+    HIPTRY(c, hipEventRecord(c->ev_user, c->user_stream));
+    HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
     c->max_rounds = a->max_rounds;
     c->rounds_launched = 0;
     const int cfg = c->cfg;
@@ -484,11 +510,9 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
         TRY(ensure(c, c->amax[k], (size_t)out_rows * 4));
     }
     if (cfg == 2) TRY(ensure(c, c->logits, (size_t)round_rows * c->V * 4));
-    if (!counts_dev) {
-        TRY(ensure(c, c->counts_own, (size_t)a->max_rounds * B * 4));
-        counts_dev = as<int32_t>(c->counts_own);
-    }
-    c->counts = counts_dev;
+    (void)counts_dev;
+    TRY(ensure(c, c->counts_own, (size_t)a->max_rounds * B * 4));
+    c->counts = as<int32_t>(c->counts_own);
     if (!c->pin) {
         HIPTRY(c, hipHostMalloc((void**)&c->pin, 64, hipHostMallocDefault));
         HIPTRY(c, hipEventCreateWithFlags(&c->ev[0], hipEventDisableTiming));
@@ -498,6 +522,10 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     // state
     std::vector<int32_t> meta(kMetaCount, 0);
     meta[kMetaRound] = -1;
+    meta[kMetaGamma] = c->gamma;
+    meta[kMetaExec] = c->exec_mode;
+    meta[kMetaSeedLo] = (int32_t)(uint32_t)c->seed;
+    meta[kMetaSeedHi] = (int32_t)(uint32_t)(c->seed >> 32);
     HIPTRY(c, hipMemcpyAsync(c->meta.p, meta.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->xtok.p, a->prefix_tokens, (size_t)B * T * 4, hipMemcpyDeviceToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->cursor.p, a->prefix_len, B * 4, hipMemcpyHostToDevice, s));
@@ -569,9 +597,9 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
                      as<int32_t>(c->pf_slots), as<float>(c->temps), 1, cfg, c->V, c->top_k,
                      c->cfg_scale, mp + kMetaOutRows, (int)pslots.size(), as<int32_t>(c->meta)};
     transform(ta, s);
-    VerifyArgs va{B, W, T, c->Hh, c->V, c->greedy, 1, 1, c->max_rounds, c->seed,
-                  as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]), nullptr,
-                  as<int32_t>(c->pf_slots), mp + kMetaImgs, (int)pslots.size(),
+    VerifyArgs va{B, W, T, c->Hh, c->V, c->greedy, 1, 1, c->max_rounds,
+                  as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
+                  nullptr, as<int32_t>(c->pf_slots), mp + kMetaImgs, (int)pslots.size(),
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
                   as<int32_t>(c->qsrc), nullptr, as<int64_t>(c->stats), as<int32_t>(c->meta)};
     verify_commit(va, s);
@@ -580,14 +608,13 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     return HBSJD_OK;
 }
 
-// queue one round (parity r & 1); every launch sizes itself from device counts
-hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
+// queue the launches of one round on buffer parity `cur`; every launch sizes
+// itself from the device counts the round's set-up kernel writes
+void enqueue_round(hbsjd_ctx* c, int cur) {
     hipStream_t s = c->stream;
-    const int r = c->rounds_launched;
-    const int cur = r & 1;
     const int B = c->B, W = c->W, cfg = c->cfg, S = B * cfg, R = W + 1;
     int32_t* mt = as<int32_t>(c->meta);
-    RoundSetupArgs sa{B, W, c->T, cfg, c->C, c->gamma, exec_mode, c->max_pages, c->max_rounds,
+    RoundSetupArgs sa{B, W, c->T, cfg, c->C, c->max_pages, c->max_rounds,
                       as<int32_t>(c->cursor), as<int32_t>(c->drafts), as<int32_t>(c->xtok),
                       as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->slot_img),
                       as<int32_t>(c->active_list), as<int32_t>(c->row_tok), as<int32_t>(c->row_pos),
@@ -606,11 +633,6 @@ hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
                         as<int32_t>(c->seg_pos0)},
                mt + kMetaSegs, S, R};
     forward_layers(c, fr);
-    {
-        Timed tm(c, HBSJD_K_NORM);
-        rmsnorm(c->bf16, as<float>(c->h), nullptr, mt + kMetaRows, rows_cap, c->g_out,
-                c->m.rms_eps, c->d, c->hb.p, s);
-    }
     float* lg = cfg == 1 ? as<float>(c->P[cur]) : as<float>(c->logits);
     {
         Timed tm(c, HBSJD_K_LMHEAD);
@@ -624,7 +646,7 @@ hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
         Timed tm(c, HBSJD_K_TRANSFORM);
         transform(ta, s);
     }
-    VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds, c->seed,
+    VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds,
                   as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
                   as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
@@ -633,8 +655,60 @@ hbsjd_status launch_round(hbsjd_ctx* c, int exec_mode) {
         Timed tm(c, HBSJD_K_VERIFY);
         verify_commit(va, s);
     }
-    HIPTRY(c, hipGetLastError());
-    c->rounds_launched = r + 1;
+}
+
+// everything a captured round bakes into its kernel arguments
+std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
+    std::vector<uint64_t> g = {(uint64_t)c->B, (uint64_t)c->W, (uint64_t)c->cfg,
+                               (uint64_t)c->Hh, (uint64_t)c->top_k, (uint64_t)c->greedy,
+                               (uint64_t)c->max_rounds, (uint64_t)c->max_pages,
+                               (uint64_t)c->kv_layer_elems};
+    uint32_t cs;
+    std::memcpy(&cs, &c->cfg_scale, 4);
+    g.push_back(cs);
+    DevBuf* bufs[] = {&c->xtok, &c->cursor, &c->drafts, &c->qsrc, &c->labels, &c->temps,
+                      &c->meta, &c->a_hist, &c->mode_hist, &c->stats, &c->counts_own,
+                      &c->row_tok, &c->row_pos, &c->row_kv, &c->row_seq, &c->seg_seq,
+                      &c->seg_row0, &c->seg_nrows, &c->seg_pos0, &c->slot_img,
+                      &c->active_list, &c->h, &c->hb, &c->qb, &c->ob, &c->act, &c->part,
+                      &c->P[0], &c->P[1], &c->CP[0], &c->CP[1], &c->amax[0], &c->amax[1],
+                      &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope};
+    for (DevBuf* b : bufs) g.push_back((uint64_t)(uintptr_t)b->p);
+    return g;
+}
+
+hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
+    for (auto& g : c->gexec)
+        if (g) {
+            HIPTRY(c, hipGraphExecDestroy(g));
+            g = nullptr;
+        }
+    c->gsig.clear();
+    for (int par = 0; par < 2; ++par) {
+        hipGraph_t graph = nullptr;
+        HIPTRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
+        enqueue_round(c, par);
+        hipError_t e = hipStreamEndCapture(c->stream, &graph);
+        if (e != hipSuccess) return hip_fail(c, e, "hipStreamEndCapture");
+        e = hipGraphInstantiate(&c->gexec[par], graph, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(graph);
+        if (e != hipSuccess) return hip_fail(c, e, "hipGraphInstantiate");
+    }
+    c->gsig = graph_signature(c);
+    return HBSJD_OK;
+}
+
+// queue one round: a graph replay, or eager launches while kernels are timed
+hbsjd_status launch_round(hbsjd_ctx* c) {
+    const int cur = c->rounds_launched & 1;
+    if (c->use_graphs && c->prof_mask == 0) {
+        if (c->gsig != graph_signature(c)) TRY(capture_round_graphs(c));
+        HIPTRY(c, hipGraphLaunch(c->gexec[cur], c->stream));
+    } else {
+        enqueue_round(c, cur);
+        HIPTRY(c, hipGetLastError());
+    }
+    c->rounds_launched += 1;
     return HBSJD_OK;
 }
 
@@ -674,13 +748,16 @@ hbsjd_status hbsjd_create(const hbsjd_model_desc* m, uint64_t max_kv_bytes, void
         c->nC = (c->V + kChunk - 1) / kChunk;
         c->bf16 = m->dtype == HBSJD_DTYPE_BF16;
         c->esz = c->bf16 ? 2 : 4;
-        c->stream = (hipStream_t)stream;
+        c->user_stream = (hipStream_t)stream;
         c->max_kv_bytes = max_kv_bytes;
         hipError_t e = hipGetDevice(&c->device);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_user, hipEventDisableTiming);
         if (e != hipSuccess) {
             delete c;
-            return fail(HBSJD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+            return fail(HBSJD_EHIP, std::string("stream set-up: ") + hipGetErrorString(e));
         }
+        if (const char* g = std::getenv("HBSJD_NO_GRAPHS")) c->use_graphs = !(g[0] == '1');
         // 2D RoPE tables: position s >= 1 is grid cell (row, col) = divmod(s - 1, G);
         // pair i < dh/4 turns by row * base^(-4i/dh), pair i >= dh/4 by
         // col * base^(-4(i - dh/4)/dh); position 0 (class token) is not turned.
@@ -837,7 +914,7 @@ hbsjd_status hbsjd_rollout(hbsjd_ctx* c, const hbsjd_rollout_args* a, hbsjd_roll
                 c->poisoned = true;
                 return fail(HBSJD_EINTERNAL, "round watchdog: rollout did not finish");
             }
-            TRY(launch_round(c, c->exec_mode));
+            TRY(launch_round(c));
             HIPTRY(c, hipMemcpyAsync(c->pin + (r & 1), as<int32_t>(c->meta) + kMetaActive, 4,
                                      hipMemcpyDeviceToHost, s));
             HIPTRY(c, hipEventRecord(c->ev[r & 1], s));
@@ -850,6 +927,8 @@ hbsjd_status hbsjd_rollout(hbsjd_ctx* c, const hbsjd_rollout_args* a, hbsjd_roll
             }
         }
         HIPTRY(c, hipMemcpyAsync(o->tokens, c->xtok.p, (size_t)c->B * c->T * 4,
+                                 hipMemcpyDeviceToDevice, s));
+        HIPTRY(c, hipMemcpyAsync(o->counts, c->counts, (size_t)c->max_rounds * c->B * 4,
                                  hipMemcpyDeviceToDevice, s));
         std::vector<int32_t> ah(rounds + 1), mh(rounds + 1);
         int64_t st[4] = {0, 0, 0, 0};
@@ -888,7 +967,13 @@ hbsjd_status hbsjd_round(hbsjd_ctx* c, int32_t exec_mode, int32_t* counts, int32
             return fail(HBSJD_EINVAL, "unknown exec_mode");
         if (c->rounds_launched >= c->max_rounds) return fail(HBSJD_ESTATE, "max_rounds reached");
         const int r = c->rounds_launched;
-        TRY(launch_round(c, exec_mode));
+        HIPTRY(c, hipEventRecord(c->ev_user, c->user_stream));
+        HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
+        c->exec_mode = exec_mode;
+        int32_t em = exec_mode;
+        HIPTRY(c, hipMemcpyAsync(as<int32_t>(c->meta) + kMetaExec, &em, 4, hipMemcpyHostToDevice,
+                                 c->stream));
+        TRY(launch_round(c));
         std::vector<int32_t> cur(c->B);
         if (counts)
             HIPTRY(c, hipMemcpyAsync(counts, c->counts + (size_t)r * c->B, c->B * 4,
@@ -955,6 +1040,8 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         hipStream_t s = c->stream;
         const int rows = row0.back();
         c->have_state = false;
+        HIPTRY(c, hipEventRecord(c->ev_user, c->user_stream));
+        HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
         TRY(ensure_acts(c, rows));
         TRY(ensure_kv(c, n_seqs, c->T + 1));
         TRY(ensure(c, c->meta, kMetaCount * 4));
@@ -1004,8 +1091,6 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
                             as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0)},
                    mp + kMetaSegs, n_seqs, maxlen};
         forward_layers(c, fr);
-        rmsnorm(c->bf16, as<float>(c->h), nullptr, mp + kMetaRows, rows, c->g_out, c->m.rms_eps,
-                c->d, c->hb.p, s);
         gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaRows, rows, logits,
                     c->b_lm, s);
         HIPTRY(c, hipGetLastError());

@@ -78,18 +78,27 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         const int page = ptab[(size_t)sq * maxp + tile];
         const uint16_t* Kb = kv + (size_t)page * page_elems + (size_t)head * 4096;
         const uint16_t* Vb = kv + (size_t)page * page_elems + (size_t)(H + head) * 4096;
+        // both operands of the tile are fetched before any MFMA so their
+        // latencies overlap
+        bf16x8_t kf[4][2], vf[4][2];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                kf[j][kk] = load_bf16x8(Kb + (j * 16 + c16) * 64 + kk * 32 + 8 * g);
+                vf[j][kk] = load_bf16x8(Vb + (j * 16 + c16) * 64 + kk * 32 + 8 * g);
+            }
         f32x4_t s[NMT][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
             for (int i = 0; i < NMT; ++i) s[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                const bf16x8_t kf = load_bf16x8(Kb + (j * 16 + c16) * 64 + kk * 32 + 8 * g);
+            for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
                 for (int i = 0; i < NMT; ++i)
-                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[i][kk], kf, s[i][j], 0, 0, 0);
-            }
+                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[i][kk], kf[j][kk], s[i][j],
+                                                                      0, 0, 0);
         }
         // online softmax; lane holds rows 4g+v of key columns c16 + 16 j
 #pragma unroll
@@ -152,10 +161,10 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
                 pf[i] = *reinterpret_cast<const bf16x8_t*>(Pw + (i * 16 + c16) * 64 + kk * 32 + 8 * g);
 #pragma unroll
             for (int dj = 0; dj < 4; ++dj) {
-                const bf16x8_t vf = load_bf16x8(Vb + (dj * 16 + c16) * 64 + kk * 32 + 8 * g);
 #pragma unroll
                 for (int i = 0; i < NMT; ++i)
-                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[i], vf, o[i][dj], 0, 0, 0);
+                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[i], vf[dj][kk], o[i][dj],
+                                                                       0, 0, 0);
             }
         }
         // the next tile overwrites P: keep its writes after these reads

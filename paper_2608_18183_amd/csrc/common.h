@@ -24,6 +24,10 @@ enum MetaSlot : int {
     kMetaMode = 5,     // 0 Full, 1 Compact
     kMetaRound = 6,    // index of the round in progress
     kMetaError = 7,    // sticky device error bits
+    kMetaGamma = 8,    // Full/Compact threshold of AUTO rounds
+    kMetaExec = 9,     // 0 AUTO, 1 FULL, 2 COMPACT
+    kMetaSeedLo = 10,  // Philox key, low and high words
+    kMetaSeedHi = 11,
     kMetaCount = 16,
 };
 
@@ -89,6 +93,10 @@ __host__ __device__ inline U4 philox4x32_10(uint64_t seed, uint32_t c0, uint32_t
 // uniform on [0, 1 - 2^-24] from the 24 high bits
 __host__ __device__ inline float unit_float(uint32_t x) {
     return (float)(x >> 8) * (1.0f / 16777216.0f);
+}
+
+__device__ inline uint64_t meta_seed(const int32_t* meta) {
+    return ((uint64_t)(uint32_t)meta[kMetaSeedHi] << 32) | (uint32_t)meta[kMetaSeedLo];
 }
 
 // the three uniforms of image b at sequence position t: draft, accept, resample

@@ -20,6 +20,10 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 // ---------------------------------------------------------------- epilogues
 // operator()(row, col, value, value of column col ^ 1 in the same row)
 
+// The bf16 kernel calls begin_tile(n0) once, row_info(m) once per output row
+// and operator()(info, m, n, value, partner) per element; the fp32 kernel only
+// uses the last two.
+
 template <typename T>
 struct EpiQkv {
     T* q;
@@ -29,16 +33,28 @@ struct EpiQkv {
     const float* rc;
     const float* rs;
     int d, heads, dh, T_;
-    __device__ void operator()(int m, int n, float v, float partner) const {
-        const int part = n / d;
+    int part = 0;   // 0 q, 1 k, 2 v: fixed per tile since d is a multiple of the tile width
+    struct Row { int p, slot; };
+    struct Aux { float cs, sn; };
+    __device__ void begin_tile(int n0) { part = n0 / d; }
+    __device__ Row row_info(int m) const {
+        int p = pos[m];
+        return Row{p > T_ ? T_ : p, kvslot[m]};
+    }
+    __device__ Aux aux(const Row& ri, int n) const {
+        if (part >= 2) return Aux{1.f, 0.f};
         const int c = n - part * d;
-        const int head = c / dh, e = c - head * dh;
+        const int e = dh == 64 ? c & 63 : c % dh;
+        const int pi = ri.p * (dh >> 1) + (e >> 1);
+        return Aux{rc[pi], rs[pi]};
+    }
+    __device__ void store(const Row& ri, const Aux& ax, int m, int n, float v, float partner) const {
+        const int c = n - part * d;
+        const int head = dh == 64 ? c >> 6 : c / dh;
+        const int e = c - head * dh;
         float out = v;
         if (part < 2) {
-            int p = pos[m];
-            p = p > T_ ? T_ : p;
-            const int pi = p * (dh >> 1) + (e >> 1);
-            const float cs = rc[pi], sn = rs[pi];
+            const float cs = ax.cs, sn = ax.sn;
             // adjacent pair (2i, 2i+1) turned by the row/column angle of position p
             out = (e & 1) ? (partner * sn + v * cs) : (v * cs - partner * sn);
         }
@@ -46,56 +62,93 @@ struct EpiQkv {
             Elem<T>::store(q + (size_t)m * d + c, out);
             return;
         }
-        const int slot = kvslot[m];
-        const int page = slot >> 6, s = slot & 63;
+        const int page = ri.slot >> 6, s = ri.slot & 63;
         const size_t base = (size_t)page * (2 * heads * 64 * dh);
         if (part == 1)
             Elem<T>::store(kv + base + (size_t)head * 64 * dh + (size_t)s * dh + e, out);
         else
             Elem<T>::store(kv + base + (size_t)(heads + head) * 64 * dh + (size_t)e * 64 + s, out);
     }
+    __device__ void operator()(int m, int n, float v, float partner) const {
+        EpiQkv e = *this;
+        e.part = n / d;
+        const Row ri = row_info(m);
+        e.store(ri, e.aux(ri, n), m, n, v, partner);
+    }
 };
 
-template <int Tag>   // 0 after the O projection, 1 after W2 (distinct kernel names)
-struct EpiResidual {
-    float* h;
+// plain fp32 store of C (split-K partials of the fp32 path)
+struct EpiStore {
+    float* out;
     int ld;
-    __device__ void operator()(int m, int n, float v, float) const {
-        float* p = h + (size_t)m * ld + n;
-        *p = *p + v;
+    struct Row {};
+    struct Aux {};
+    __device__ void begin_tile(int) {}
+    __device__ Row row_info(int) const { return Row{}; }
+    __device__ Aux aux(const Row&, int) const { return Aux{}; }
+    __device__ void store(const Row&, const Aux&, int m, int n, float v, float) const {
+        out[(size_t)m * ld + n] = v;
     }
+    __device__ void operator()(const Row& r, int m, int n, float v, float p) const {
+        store(r, Aux{}, m, n, v, p);
+    }
+    __device__ void operator()(int m, int n, float v, float p) const { (*this)(Row{}, m, n, v, p); }
 };
 
 template <typename T>
 struct EpiSwiGLU {
     T* act;
     int ld;   // f
+    struct Row {};
+    struct Aux {};
+    __device__ void begin_tile(int) {}
+    __device__ Row row_info(int) const { return Row{}; }
+    __device__ Aux aux(const Row&, int) const { return Aux{}; }
     // columns 2i / 2i+1 are the gate (W1 row i) and the up projection (W3 row i)
-    __device__ void operator()(int m, int n, float v, float partner) const {
+    __device__ void store(const Row&, const Aux&, int m, int n, float v, float partner) const {
         if (n & 1) return;
         const float silu = v / (1.0f + __expf(-v));
         Elem<T>::store(act + (size_t)m * ld + (n >> 1), silu * partner);
     }
+    __device__ void operator()(const Row& r, int m, int n, float v, float p) const {
+        store(r, Aux{}, m, n, v, p);
+    }
+    __device__ void operator()(int m, int n, float v, float p) const { (*this)(Row{}, m, n, v, p); }
 };
 
 struct EpiLogits {
     float* out;
     const float* bias;
     int ld;
-    __device__ void operator()(int m, int n, float v, float) const {
-        out[(size_t)m * ld + n] = bias ? v + bias[n] : v;
+    struct Row {};
+    struct Aux { float b; };
+    __device__ void begin_tile(int) {}
+    __device__ Row row_info(int) const { return Row{}; }
+    __device__ Aux aux(const Row&, int n) const { return Aux{bias ? bias[n] : 0.f}; }
+    __device__ void store(const Row&, const Aux& ax, int m, int n, float v, float) const {
+        out[(size_t)m * ld + n] = v + ax.b;
     }
+    __device__ void operator()(const Row& r, int m, int n, float v, float p) const {
+        store(r, aux(r, n), m, n, v, p);
+    }
+    __device__ void operator()(int m, int n, float v, float p) const { (*this)(Row{}, m, n, v, p); }
 };
 
 // ---------------------------------------------------------------- bf16 MFMA
-
-template <int BM, int BN, typename Epi>
+// Workgroup tile BM x BN, 4 wavefronts arranged WGM x WGN, 64-deep K steps.
+// Tiles are staged global -> registers -> LDS (XOR-swizzled 16-byte chunks,
+// double-buffered); NS register stages keep NS-1 tiles in flight so a step
+// does not wait a full memory round trip. With splits > 1 the K range is cut
+// into equal contiguous parts and each part writes fp32 partial sums to
+// `part` ([split][M][N]) instead of calling the epilogue; the caller's reduce
+// kernel adds the parts in split order.
+template <int BM, int BN, int WGM, int WGN, int NS, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
                                                    const uint16_t* __restrict__ W, int N, int K,
                                                    const int* __restrict__ m_dev, int m_cap,
-                                                   Epi epi) {
+                                                   int splits, float* __restrict__ part, Epi epi) {
     constexpr int BK = 64;
-    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 16, TN = WN / 16;
     constexpr int LA = BM / 32, LB = BN / 32;   // 16-byte chunks per thread per tile
     __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * BK];
@@ -103,47 +156,49 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 
     const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
     const int tiles_m = (m_cap + BM - 1) / BM;
-    const int total = tiles_m * (N / BN);
+    const int total = tiles_m * (N / BN) * splits;
     const int per_xcd = (total + 7) >> 3;
-    // workgroups are dealt to the 8 XCDs round-robin; give each XCD a contiguous
-    // range of tiles (all M tiles of a few N tiles) so it reuses weight tiles in its L2
+    // workgroups are dealt to the 8 XCDs round-robin; each XCD gets a contiguous
+    // range of tiles (all M tiles of a few (N tile, split) pairs) so it reuses
+    // weight tiles in its own L2
     const int lin = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
     if (lin >= total) return;
-    const int tn = lin / tiles_m, tm = lin - tn * tiles_m;
+    const int tm = lin % tiles_m;
+    const int nz = lin / tiles_m;
+    const int z = nz % splits, tn = nz / splits;
     const int m0 = tm * BM, n0 = tn * BN;
     if (m0 >= M) return;
+    const int Ks = K / splits;
+    const int kbase = z * Ks;
+    const int nk = Ks / BK;
 
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    const int wm = wv >> 1, wn = wv & 1;
+    const int wm = wv / WGN, wn = wv % WGN;
     const int lc = t & 7, lr = t >> 3;
 
-    uint4 ra[LA], rb[LB];
-    auto gload = [&](int k0) {
+    uint4 R[NS][LA + LB];
+    auto gload = [&](uint4* r, int kt) {
+        const int k0 = kbase + kt * BK;
 #pragma unroll
         for (int i = 0; i < LA; ++i) {
-            const int r = lr + 32 * i;
-            const int gm = m0 + r;
-            if (gm < M)
-                ra[i] = *reinterpret_cast<const uint4*>(A + (size_t)gm * lda + k0 + lc * 8);
-            else
-                ra[i] = make_uint4(0, 0, 0, 0);
+            const int gm = m0 + lr + 32 * i;
+            r[i] = gm < M ? *reinterpret_cast<const uint4*>(A + (size_t)gm * lda + k0 + lc * 8)
+                          : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < LB; ++i) {
-            const int r = lr + 32 * i;
-            rb[i] = *reinterpret_cast<const uint4*>(W + (size_t)(n0 + r) * K + k0 + lc * 8);
-        }
+        for (int i = 0; i < LB; ++i)
+            r[LA + i] = *reinterpret_cast<const uint4*>(W + (size_t)(n0 + lr + 32 * i) * K + k0 + lc * 8);
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](const uint4* r, int buf) {
 #pragma unroll
         for (int i = 0; i < LA; ++i) {
-            const int r = lr + 32 * i;
-            *reinterpret_cast<uint4*>(&As[buf][r * BK + ((lc ^ (r & 7)) << 3)]) = ra[i];
+            const int row = lr + 32 * i;
+            *reinterpret_cast<uint4*>(&As[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[i];
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
-            const int r = lr + 32 * i;
-            *reinterpret_cast<uint4*>(&Bs[buf][r * BK + ((lc ^ (r & 7)) << 3)]) = rb[i];
+            const int row = lr + 32 * i;
+            *reinterpret_cast<uint4*>(&Bs[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[LA + i];
         }
     };
 
@@ -153,13 +208,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = K / BK;
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload((kt + 1) * BK);
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             const int ch = kk * 4 + (lane >> 4);
@@ -181,46 +230,95 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j],
                                                                         0, 0, 0);
         }
-        if (kt + 1 < nk) sstore(buf ^ 1);
-        __syncthreads();
+    };
+
+    // tile kt lives in register stage kt % NS; stage s is refilled with tile
+    // kt + NS - 1 once its previous tile went to LDS
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nk) gload(R[s], s);
+    sstore(R[0], 0);
+    __syncthreads();
+    for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int kt = kt0 + s;
+            if (kt < nk) {
+                if (kt + NS - 1 < nk) gload(R[(s + NS - 1) % NS], kt + NS - 1);
+                compute(kt & 1);
+                if (kt + 1 < nk) sstore(R[(s + 1) % NS], (kt + 1) & 1);
+                __syncthreads();
+            }
+        }
     }
 
     // 16x16 accumulator layout: lane holds rows 4*(lane/16)+v of column lane%16
+    const int col0 = n0 + wn * WN + (lane & 15);
+    if (splits > 1) {
+        float* P = part + (size_t)z * m_cap * N;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+                if (row >= M) continue;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
+            }
+        return;
+    }
+    // epilogue in two phases: every load the epilogue needs (row metadata, tables)
+    // first, then the arithmetic and the stores, so no store sits between loads
+    epi.begin_tile(n0);
+    typename Epi::Row rinfo[TM][4];
+    typename Epi::Aux aux[TM][4][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int v = 0; v < 4; ++v) {
+            const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+            rinfo[i][v] = epi.row_info(row < M ? row : 0);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
+            for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
+        }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+            const bool ok = row < M;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
                 const float val = acc[i][j][v];
                 const float partner = __shfl_xor(val, 1, 64);
-                const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
-                const int col = n0 + wn * WN + j * 16 + (lane & 15);
-                if (row < M) epi(row, col, val, partner);
+                if (ok) epi.store(rinfo[i][v], aux[i][v][j], row, col0 + j * 16, val, partner);
             }
+        }
 }
 
-template <int BM, int BN, typename Epi>
+template <int BM, int BN, int WGM, int WGN, typename Epi>
 static void launch_bf16(const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-                        int m_cap, const Epi& epi, hipStream_t s) {
+                        int m_cap, int splits, float* part, const Epi& epi, hipStream_t s) {
     if (m_cap <= 0) return;
-    const int tiles = ((m_cap + BM - 1) / BM) * (N / BN);
+    const int tiles = ((m_cap + BM - 1) / BM) * (N / BN) * splits;
     const int grid = ((tiles + 7) / 8) * 8;
-    launch(k_gemm_bf16<BM, BN, Epi>, dim3(grid), dim3(256), 0, s,
-                       (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, epi);
+    // deep register staging for the small tiles of the weight-streaming rounds;
+    // the large tiles have enough MFMA work per step to cover a shallower pipeline
+    constexpr int NS = BM * BN >= 128 * 128 ? 2 : 4;
+    launch(k_gemm_bf16<BM, BN, WGM, WGN, NS, Epi>, dim3(grid), dim3(256), 0, s,
+           (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
 }
 
-// tile choice: enough workgroups to cover the 256 CUs at the launch's row cap
+// tile choice by the launch's row cap (the same for Full and Compact rounds):
+// large tiles once there are enough of them to fill the 256 CUs twice over
 template <typename Epi>
 static void dispatch_bf16(const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-                          int m_cap, const Epi& epi, hipStream_t s) {
-    const long big = (long)((m_cap + 127) / 128) * (N / 128);
-    if (N % 128 == 0 && big >= 512)
-        launch_bf16<128, 128>(A, lda, W, N, K, m_dev, m_cap, epi, s);
-    else if (N % 128 == 0 && (long)((m_cap + 63) / 64) * (N / 128) >= 256)
-        launch_bf16<64, 128>(A, lda, W, N, K, m_dev, m_cap, epi, s);
+                          int m_cap, int splits, float* part, const Epi& epi, hipStream_t s) {
+    const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
+    if (N % 128 == 0 && t128 >= 512)
+        launch_bf16<128, 128, 2, 2>(A, lda, W, N, K, m_dev, m_cap, splits, part, epi, s);
     else
-        launch_bf16<64, 64>(A, lda, W, N, K, m_dev, m_cap, epi, s);
+        launch_bf16<64, 64, 2, 2>(A, lda, W, N, K, m_dev, m_cap, splits, part, epi, s);
 }
 
 // ---------------------------------------------------------------- fp32
@@ -285,12 +383,25 @@ static void launch_f32(const void* A, int lda, const void* W, int N, int K, cons
 
 // ---------------------------------------------------------------- entry points
 
+int split_for(int m_cap, int N, int K) {
+    // enough (tile, split) pairs for about two 64x64 workgroups per CU, at most
+    // four parts, each a whole number of 64-deep steps
+    const long tiles = (long)((m_cap + 63) / 64) * (N / 64);
+    int want = (int)((512 + tiles - 1) / tiles);
+    want = want < 1 ? 1 : (want > 4 ? 4 : want);
+    const int steps = K / 64;
+    int sp = 1;
+    for (int c = 1; c <= want; ++c)
+        if (steps % c == 0) sp = c;
+    return sp;
+}
+
 void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
               int m_cap, const QkvArgs& e, hipStream_t s) {
     if (bf16) {
         EpiQkv<uint16_t> epi{(uint16_t*)e.q, (uint16_t*)e.kv, e.pos, e.kvslot, e.rope_cos,
                              e.rope_sin, e.d, e.heads, e.head_dim, e.T};
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, epi, s);
+        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
     } else {
         EpiQkv<float> epi{(float*)e.q, (float*)e.kv, e.pos, e.kvslot, e.rope_cos, e.rope_sin,
                           e.d, e.heads, e.head_dim, e.T};
@@ -298,29 +409,41 @@ void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, co
     }
 }
 
+template <int Tag>   // 0 the O projection, 1 W2 (distinct kernel names in traces)
+struct PartialTag {};
+
 template <int Tag>
-static void residual_tag(bool bf16, const void* A, int lda, const void* W, int N, int K,
-                         const int* m_dev, int m_cap, float* h, hipStream_t s) {
-    EpiResidual<Tag> epi{h, N};
-    if (bf16)
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, epi, s);
-    else
-        launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
+static void partial_tag(bool bf16, const void* A, int lda, const void* W, int N, int K,
+                        const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
+    if (bf16) {
+        struct EpiNone {
+            struct Row {};
+            struct Aux {};
+            __device__ void begin_tile(int) {}
+            __device__ Row row_info(int) const { return Row{}; }
+            __device__ Aux aux(const Row&, int) const { return Aux{}; }
+            __device__ void store(const Row&, const Aux&, int, int, float, float) const {}
+            PartialTag<Tag> tag;
+        };
+        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, splits, part, EpiNone{}, s);
+    } else {
+        launch_f32(A, lda, W, N, K, m_dev, m_cap, EpiStore{part, N}, s);
+    }
 }
 
-void gemm_residual(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
-                   const int* m_dev, int m_cap, float* h, hipStream_t s) {
+void gemm_partial(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
+                  const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
     if (tag == 0)
-        residual_tag<0>(bf16, A, lda, W, N, K, m_dev, m_cap, h, s);
+        partial_tag<0>(bf16, A, lda, W, N, K, m_dev, m_cap, splits, part, s);
     else
-        residual_tag<1>(bf16, A, lda, W, N, K, m_dev, m_cap, h, s);
+        partial_tag<1>(bf16, A, lda, W, N, K, m_dev, m_cap, splits, part, s);
 }
 
 void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s) {
     if (bf16) {
         EpiSwiGLU<uint16_t> epi{(uint16_t*)act, N / 2};
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, epi, s);
+        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
     } else {
         EpiSwiGLU<float> epi{(float*)act, N / 2};
         launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
@@ -331,7 +454,7 @@ void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
                  const int* m_dev, int m_cap, float* out, const float* bias, hipStream_t s) {
     EpiLogits epi{out, bias, N};
     if (bf16)
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, epi, s);
+        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
     else
         launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
 }

@@ -67,8 +67,11 @@ struct QkvArgs {
 
 void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
               int m_cap, const QkvArgs& e, hipStream_t s);
-void gemm_residual(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
-                   const int* m_dev, int m_cap, float* h, hipStream_t s);
+// split-K partial sums part[split][m_cap][N] (tag 0: O projection, 1: W2);
+// split_for() is the split count the host must size `part` for
+int split_for(int m_cap, int N, int K);
+void gemm_partial(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
+                  const int* m_dev, int m_cap, int splits, float* part, hipStream_t s);
 void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s);
 void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
@@ -86,9 +89,14 @@ void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_
                 float* h, void* hb, hipStream_t s);
 void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s);
+// h += sum over splits (in split order) of part[split][m_cap][d]; then
+// hb = RMSNorm(h) * gain (hb may be null)
+void reduce_residual_norm(bool bf16, const float* part, int splits, int m_cap, float* h,
+                          const int* nrows_dev, const float* gain, float eps, int d, void* hb,
+                          hipStream_t s);
 
 struct RoundSetupArgs {
-    int B, W, T, cfg, C, gamma, exec_mode, max_pages, max_rounds;
+    int B, W, T, cfg, C, max_pages, max_rounds;   // gamma and exec mode come from meta
     const int32_t* cursor;
     const int32_t* drafts;
     const int32_t* xtok;
@@ -145,8 +153,7 @@ struct TransformArgs {
 void transform(const TransformArgs& a, hipStream_t s);
 
 struct VerifyArgs {
-    int B, W, T, H, V, greedy, prefill, rows_per_slot, max_rounds;
-    uint64_t seed;
+    int B, W, T, H, V, greedy, prefill, rows_per_slot, max_rounds;   // seed comes from meta
     const float* p;          // this round's distribution rows
     const float* cprefix;
     const int32_t* amax;

@@ -43,10 +43,11 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
         __syncthreads();
     }
     const int A = s_base;
+    const int exec_mode = a.meta[kMetaExec];
     int mode;
-    if (a.exec_mode == 1) mode = 0;
-    else if (a.exec_mode == 2) mode = 1;
-    else mode = A > a.gamma ? 0 : 1;
+    if (exec_mode == 1) mode = 0;
+    else if (exec_mode == 2) mode = 1;
+    else mode = A > a.meta[kMetaGamma] ? 0 : 1;
     const int nimg = A == 0 ? 0 : (mode == 0 ? a.B : A);
     const int R = a.W + 1;
     const int rows = nimg * a.cfg * R;
@@ -151,68 +152,176 @@ void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V
 }
 
 // ---------------------------------------------------------------- norms
-// RMSNorm(x) * g = x * (1 / sqrt(mean(x^2) + eps)) * g, one 256-thread block per row.
+// RMSNorm(x) * g = x * (1 / sqrt(mean(x^2) + eps)) * g. One wavefront per row,
+// four rows per 256-thread block; the row stays in registers (d <= 64 * kMaxPer).
+
+constexpr int kMaxPer = 24;   // d <= 1536
 
 template <typename T>
-__device__ inline void norm_row(const float* x, const float* g, float eps, int d, T* out,
-                                float* red) {
+__device__ inline void norm_store(const float* x, int per, const float* __restrict__ g, float eps,
+                                  int d, T* __restrict__ out) {
+    const int lane = threadIdx.x & 63;
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss = fmaf(x[i], x[i], ss);
-    ss = block_reduce(ss, red, [](float u, float v) { return u + v; });
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k)
+        if (k < per) ss = fmaf(x[k], x[k], ss);
+    ss = wave_sum(ss);
     const float r = 1.0f / sqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; i < d; i += 256) Elem<T>::store(out + i, (x[i] * r) * g[i]);
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k) {
+        const int i = lane + 64 * k;
+        if (k < per && i < d) Elem<T>::store(out + i, (x[k] * r) * g[i]);
+    }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nrows_dev,
-                                                    const T* tok_emb, const T* cls_emb,
-                                                    const float* g, float eps, int d, float* h,
-                                                    T* hb) {
-    __shared__ float red[4];
-    const int r = blockIdx.x;
+                                                    const T* __restrict__ tok_emb,
+                                                    const T* __restrict__ cls_emb,
+                                                    const float* __restrict__ g, float eps, int d,
+                                                    float* __restrict__ h, T* __restrict__ hb) {
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (r >= *nrows_dev) return;
     const int tok = rows.tok[r];
     const T* e = tok >= 0 ? tok_emb + (size_t)tok * d : cls_emb + (size_t)(-(tok + 1)) * d;
-    float* hr = h + (size_t)r * d;
-    for (int i = threadIdx.x; i < d; i += 256) hr[i] = Elem<T>::load(e + i);
-    __syncthreads();
-    norm_row(hr, g, eps, d, hb + (size_t)r * d, red);
+    const int per = (d + 63) / 64;
+    float x[kMaxPer];
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k) {
+        const int i = lane + 64 * k;
+        x[k] = (k < per && i < d) ? Elem<T>::load(e + i) : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k) {
+        const int i = lane + 64 * k;
+        if (k < per && i < d) h[(size_t)r * d + i] = x[k];
+    }
+    norm_store(x, per, g, eps, d, hb + (size_t)r * d);
 }
 
 void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
                 const void* tok_emb, const void* cls_emb, const float* gain, float eps, int d,
                 float* h, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
+    const dim3 grid((nrows_cap + 3) / 4);
     if (bf16)
-        launch(k_embed_norm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, rows,
-                           nrows_dev, (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain,
-                           eps, d, h, (uint16_t*)hb);
+        launch(k_embed_norm<uint16_t>, grid, dim3(256), 0, s, rows, nrows_dev,
+               (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain, eps, d, h, (uint16_t*)hb);
     else
-        launch(k_embed_norm<float>, dim3(nrows_cap), dim3(256), 0, s, rows, nrows_dev,
-                           (const float*)tok_emb, (const float*)cls_emb, gain, eps, d, h,
-                           (float*)hb);
+        launch(k_embed_norm<float>, grid, dim3(256), 0, s, rows, nrows_dev, (const float*)tok_emb,
+               (const float*)cls_emb, gain, eps, d, h, (float*)hb);
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* h, const int32_t* src_idx,
-                                                 const int* nrows_dev, const float* g, float eps,
-                                                 int d, T* hb) {
-    __shared__ float red[4];
-    const int r = blockIdx.x;
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
+                                                 const int32_t* src_idx, const int* nrows_dev,
+                                                 const float* __restrict__ g, float eps, int d,
+                                                 T* __restrict__ hb) {
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
     if (r >= *nrows_dev) return;
     const int src = src_idx ? src_idx[r] : r;
-    norm_row(h + (size_t)src * d, g, eps, d, hb + (size_t)r * d, red);
+    const int per = (d + 63) / 64;
+    float x[kMaxPer];
+#pragma unroll
+    for (int k = 0; k < kMaxPer; ++k) {
+        const int i = lane + 64 * k;
+        x[k] = (k < per && i < d) ? h[(size_t)src * d + i] : 0.f;
+    }
+    norm_store(x, per, g, eps, d, hb + (size_t)r * d);
 }
 
 void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
+    const dim3 grid((nrows_cap + 3) / 4);
     if (bf16)
-        launch(k_rmsnorm<uint16_t>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
-                           nrows_dev, gain, eps, d, (uint16_t*)hb);
+        launch(k_rmsnorm<uint16_t>, grid, dim3(256), 0, s, h, src_idx, nrows_dev, gain, eps, d,
+               (uint16_t*)hb);
     else
-        launch(k_rmsnorm<float>, dim3(nrows_cap), dim3(256), 0, s, h, src_idx,
-                           nrows_dev, gain, eps, d, (float*)hb);
+        launch(k_rmsnorm<float>, grid, dim3(256), 0, s, h, src_idx, nrows_dev, gain, eps, d,
+               (float*)hb);
+}
+
+template <typename T, int PER>
+__global__ __launch_bounds__(256) void k_reduce_norm(const float* __restrict__ part, int splits,
+                                                     int m_cap, float* __restrict__ h,
+                                                     const int* nrows_dev,
+                                                     const float* __restrict__ g, float eps, int d,
+                                                     T* __restrict__ hb) {
+    constexpr int kSplitMax = 4;
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (r >= min(*nrows_dev, m_cap)) return;
+    // one phase of loads: every split's partial, the residual and the gain
+    float pz[kSplitMax][PER], hv[PER], gv[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = lane + 64 * k;
+        const bool in = i < d;
+#pragma unroll
+        for (int z = 0; z < kSplitMax; ++z)
+            pz[z][k] = (in && z < splits) ? part[((size_t)z * m_cap + r) * d + i] : 0.f;
+        hv[k] = in ? h[(size_t)r * d + i] : 0.f;
+        gv[k] = in ? g[i] : 0.f;
+    }
+    float x[PER];
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        float acc = pz[0][k];
+#pragma unroll
+        for (int z = 1; z < kSplitMax; ++z)
+            if (z < splits) acc += pz[z][k];    // split order
+        x[k] = hv[k] + acc;
+        ss = fmaf(x[k], x[k], ss);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = lane + 64 * k;
+        if (i < d) h[(size_t)r * d + i] = x[k];
+    }
+    if (!hb) return;
+    ss = wave_sum(ss);
+    const float rn = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = lane + 64 * k;
+        if (i < d) Elem<T>::store(hb + (size_t)r * d + i, (x[k] * rn) * gv[k]);
+    }
+}
+
+template <typename T, int PER>
+static void reduce_norm_launch(const float* part, int splits, int m_cap, float* h,
+                               const int* nrows_dev, const float* gain, float eps, int d, void* hb,
+                               hipStream_t s) {
+    launch(k_reduce_norm<T, PER>, dim3((m_cap + 3) / 4), dim3(256), 0, s, part, splits, m_cap, h,
+           nrows_dev, gain, eps, d, (T*)hb);
+}
+
+template <typename T>
+static void reduce_norm_dispatch(const float* part, int splits, int m_cap, float* h,
+                                 const int* nrows_dev, const float* gain, float eps, int d,
+                                 void* hb, hipStream_t s) {
+    const int per = (d + 63) / 64;
+    if (per <= 1)
+        reduce_norm_launch<T, 1>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else if (per <= 4)
+        reduce_norm_launch<T, 4>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else if (per <= 12)
+        reduce_norm_launch<T, 12>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else if (per <= 16)
+        reduce_norm_launch<T, 16>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else
+        reduce_norm_launch<T, 24>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+}
+
+void reduce_residual_norm(bool bf16, const float* part, int splits, int m_cap, float* h,
+                          const int* nrows_dev, const float* gain, float eps, int d, void* hb,
+                          hipStream_t s) {
+    if (m_cap <= 0) return;
+    if (bf16)
+        reduce_norm_dispatch<uint16_t>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else
+        reduce_norm_dispatch<float>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
 }
 
 // ---------------------------------------------------------------- Philox test entry

@@ -364,6 +364,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     if (n >= a.T) return;              // finished image in Full mode: rows discarded
     const int W = a.W, V = a.V, R = a.rows_per_slot;
     const int nC = (V + kChunk - 1) / kChunk;
+    const uint64_t seed = meta_seed(a.meta);
     int n_new, base, nrows;
     if (a.prefill) {
         n_new = n;
@@ -389,7 +390,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
                 const int qs = old_q[t];
                 const float Q = qs >= 0 ? a.p_prev[(size_t)qs * V + z] : 1.0f;
                 if (!(Q > 0.f)) atomicOr(&a.meta[kMetaError], (int)kErrZeroProposal);
-                const float u = uniforms_at(a.seed, b, n + j).acc;
+                const float u = uniforms_at(seed, b, n + j).acc;
                 acc = (P >= Q) || (u < P / Q);
             }
             if (!acc) atomicMin(&s_first, j);
@@ -408,7 +409,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
                 const int qs = old_q[js - 1];
                 const int z = old_dr[js - 1];
                 const float* qr = qs >= 0 ? a.p_prev + (size_t)qs * V : nullptr;
-                const float u = uniforms_at(a.seed, b, n + js).res;
+                const float u = uniforms_at(seed, b, n + js).res;
                 rep = block_inv_cdf(
                     [=](int v) {
                         const float qv = qr ? qr[v] : (v == z ? 1.0f : 0.0f);
@@ -464,7 +465,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
             z = a.amax[prow];
         else
             z = wave_sample_cp(a.p + (size_t)prow * V, a.cprefix + (size_t)prow * (nC + 1), V, nC,
-                               uniforms_at(a.seed, b, pos).draft);
+                               uniforms_at(seed, b, pos).draft);
         if (lane == 0) {
             new_dr[m - 1] = z;
             new_q[m - 1] = prow;
