@@ -16,6 +16,9 @@ namespace hbsjd {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+// 16-byte staging chunk as a first-class vector (a copy of HIP's uint4 struct
+// becomes a memcpy that keeps the stage arrays out of registers)
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
 // ---------------------------------------------------------------- epilogues
 // operator()(row, col, value, value of column col ^ 1 in the same row)
@@ -41,11 +44,12 @@ struct EpiQkv {
         int p = pos[m];
         return Row{p > T_ ? T_ : p, kvslot[m]};
     }
+    // loads unconditionally (the V part reads an entry it ignores) so the GEMM's
+    // load pipeline sees the same number of loads on every path
     __device__ Aux aux(const Row& ri, int n) const {
-        if (part >= 2) return Aux{1.f, 0.f};
         const int c = n - part * d;
         const int e = dh == 64 ? c & 63 : c % dh;
-        const int pi = ri.p * (dh >> 1) + (e >> 1);
+        const int pi = part < 2 ? ri.p * (dh >> 1) + (e >> 1) : 0;
         return Aux{rc[pi], rs[pi]};
     }
     __device__ void store(const Row& ri, const Aux& ax, int m, int n, float v, float partner) const {
@@ -116,6 +120,7 @@ struct EpiSwiGLU {
     __device__ void operator()(int m, int n, float v, float p) const { (*this)(Row{}, m, n, v, p); }
 };
 
+template <bool Bias>
 struct EpiLogits {
     float* out;
     const float* bias;
@@ -124,7 +129,7 @@ struct EpiLogits {
     struct Aux { float b; };
     __device__ void begin_tile(int) {}
     __device__ Row row_info(int) const { return Row{}; }
-    __device__ Aux aux(const Row&, int n) const { return Aux{bias ? bias[n] : 0.f}; }
+    __device__ Aux aux(const Row&, int n) const { return Aux{Bias ? bias[n] : 0.f}; }
     __device__ void store(const Row&, const Aux& ax, int m, int n, float v, float) const {
         out[(size_t)m * ld + n] = v + ax.b;
     }
@@ -137,11 +142,18 @@ struct EpiLogits {
 // ---------------------------------------------------------------- bf16 MFMA
 // Workgroup tile BM x BN, 4 wavefronts arranged WGM x WGN, 64-deep K steps.
 // Tiles are staged global -> registers -> LDS (XOR-swizzled 16-byte chunks,
-// double-buffered); NS register stages keep NS-1 tiles in flight so a step
-// does not wait a full memory round trip. With splits > 1 the K range is cut
-// into equal contiguous parts and each part writes fp32 partial sums to
-// `part` ([split][M][N]) instead of calling the epilogue; the caller's reduce
-// kernel adds the parts in split order.
+// double-buffered); NS register stages keep NS-2 tiles in flight behind the
+// one being written to LDS, so a step does not wait a full memory round trip.
+// That only holds if every step issues the same loads on every path: the
+// compiler's wait counts are per wavefront and in issue order, and a load
+// skipped on some path forces it to wait for everything. So the steady loop
+// has no conditional loads: rows past M re-read row M-1 (their products land
+// in rows that are never stored) and steps past the end re-read the last K
+// tile. The epilogue's own inputs (row metadata, RoPE tables, bias) are
+// fetched before the main loop so their latency hides behind it.
+// With splits > 1 the K range is cut into equal contiguous parts and each part
+// writes fp32 partial sums to `part` ([split][M][N]) instead of calling the
+// epilogue; the caller's reduce kernel adds the parts in split order.
 template <int BM, int BN, int WGM, int WGN, int NS, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
                                                    const uint16_t* __restrict__ W, int N, int K,
@@ -176,29 +188,29 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     const int wm = wv / WGN, wn = wv % WGN;
     const int lc = t & 7, lr = t >> 3;
 
-    uint4 R[NS][LA + LB];
-    auto gload = [&](uint4* r, int kt) {
+    u32x4_t R[NS][LA + LB];
+    auto gload = [&](u32x4_t* r, int kt) {
+        kt = kt < nk ? kt : nk - 1;
         const int k0 = kbase + kt * BK;
 #pragma unroll
         for (int i = 0; i < LA; ++i) {
-            const int gm = m0 + lr + 32 * i;
-            r[i] = gm < M ? *reinterpret_cast<const uint4*>(A + (size_t)gm * lda + k0 + lc * 8)
-                          : make_uint4(0, 0, 0, 0);
+            const int gm = min(m0 + lr + 32 * i, M - 1);
+            r[i] = *reinterpret_cast<const u32x4_t*>(A + (size_t)gm * lda + k0 + lc * 8);
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i)
-            r[LA + i] = *reinterpret_cast<const uint4*>(W + (size_t)(n0 + lr + 32 * i) * K + k0 + lc * 8);
+            r[LA + i] = *reinterpret_cast<const u32x4_t*>(W + (size_t)(n0 + lr + 32 * i) * K + k0 + lc * 8);
     };
-    auto sstore = [&](const uint4* r, int buf) {
+    auto sstore = [&](const u32x4_t* r, int buf) {
 #pragma unroll
         for (int i = 0; i < LA; ++i) {
             const int row = lr + 32 * i;
-            *reinterpret_cast<uint4*>(&As[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[i];
+            *reinterpret_cast<u32x4_t*>(&As[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[i];
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
             const int row = lr + 32 * i;
-            *reinterpret_cast<uint4*>(&Bs[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[LA + i];
+            *reinterpret_cast<u32x4_t*>(&Bs[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[LA + i];
         }
     };
 
@@ -232,28 +244,57 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
         }
     };
 
-    // tile kt lives in register stage kt % NS; stage s is refilled with tile
-    // kt + NS - 1 once its previous tile went to LDS
+    // epilogue inputs: row metadata first, then the first tiles, then the
+    // per-element tables that depend on the row metadata
+    const int col0 = n0 + wn * WN + (lane & 15);
+    constexpr bool kPrefetchAux = TM * TN <= 4;
+    epi.begin_tile(n0);
+    typename Epi::Row rinfo[TM][4];
+    typename Epi::Aux aux[TM][4][TN];
+    // (the split-K partial epilogue loads nothing, so this is free there)
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-        if (s < nk) gload(R[s], s);
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            rinfo[i][v] = epi.row_info(min(m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v, M - 1));
+    // tile kt lives in register stage kt % NS
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) gload(R[s], s);
+    if (kPrefetchAux) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
+    }
     sstore(R[0], 0);
     __syncthreads();
-    for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+    // steady state: step kt loads tile kt+NS-1 into the stage tile kt-1 left,
+    // computes tile kt and moves tile kt+1 from registers to the other buffer
+    const int nk_main = nk - nk % NS;
+    for (int kt0 = 0; kt0 < nk_main; kt0 += NS) {
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int kt = kt0 + s;
-            if (kt < nk) {
-                if (kt + NS - 1 < nk) gload(R[(s + NS - 1) % NS], kt + NS - 1);
-                compute(kt & 1);
-                if (kt + 1 < nk) sstore(R[(s + 1) % NS], (kt + 1) & 1);
-                __syncthreads();
-            }
+            gload(R[(s + NS - 1) % NS], kt + NS - 1);
+            compute(kt & 1);
+            sstore(R[(s + 1) % NS], (kt + 1) & 1);
+            __syncthreads();
+        }
+    }
+    // the last nk % NS steps: their tiles were loaded by the steady loop
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) {
+        const int kt = nk_main + s;
+        if (kt < nk) {
+            compute(kt & 1);
+            if (kt + 1 < nk) sstore(R[(s + 1) % NS], (kt + 1) & 1);
+            __syncthreads();
         }
     }
 
     // 16x16 accumulator layout: lane holds rows 4*(lane/16)+v of column lane%16
-    const int col0 = n0 + wn * WN + (lane & 15);
     if (splits > 1) {
         float* P = part + (size_t)z * m_cap * N;
 #pragma unroll
@@ -267,20 +308,14 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
             }
         return;
     }
-    // epilogue in two phases: every load the epilogue needs (row metadata, tables)
-    // first, then the arithmetic and the stores, so no store sits between loads
-    epi.begin_tile(n0);
-    typename Epi::Row rinfo[TM][4];
-    typename Epi::Aux aux[TM][4][TN];
+    if (!kPrefetchAux) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
-            rinfo[i][v] = epi.row_info(row < M ? row : 0);
+            for (int v = 0; v < 4; ++v)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
-        }
+                for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -304,7 +339,7 @@ static void launch_bf16(const void* A, int lda, const void* W, int N, int K, con
     const int grid = ((tiles + 7) / 8) * 8;
     // deep register staging for the small tiles of the weight-streaming rounds;
     // the large tiles have enough MFMA work per step to cover a shallower pipeline
-    constexpr int NS = BM * BN >= 128 * 128 ? 2 : 4;
+    constexpr int NS = BM * BN >= 128 * 128 ? 3 : 4;
     launch(k_gemm_bf16<BM, BN, WGM, WGN, NS, Epi>, dim3(grid), dim3(256), 0, s,
            (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
 }
@@ -452,11 +487,19 @@ void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
 
 void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
                  const int* m_dev, int m_cap, float* out, const float* bias, hipStream_t s) {
-    EpiLogits epi{out, bias, N};
-    if (bf16)
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
-    else
-        launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
+    if (bias) {
+        EpiLogits<true> epi{out, bias, N};
+        if (bf16)
+            dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        else
+            launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
+    } else {
+        EpiLogits<false> epi{out, nullptr, N};
+        if (bf16)
+            dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        else
+            launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
+    }
 }
 
 }  // namespace hbsjd
