@@ -133,6 +133,8 @@ def main() -> int:
     ap.add_argument("--gamma", type=int, default=-1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=0, help="images in the CPU sample (0 = auto)")
+    ap.add_argument("--ar-steps", type=int, default=2,
+                    help="timed rollouts of the cached-AR baseline after the SJD ones (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the rollout shards by image with no "
@@ -195,6 +197,25 @@ def main() -> int:
     dom_ms, dom_n = ctx.hbsjd_profile_read()[dominant]
     ctx.hbsjd_profile_start(())
 
+    # the cached-AR baseline on the same batch (one row per image per round),
+    # timed after the SJD region with the same clock
+    ar = None
+    if args.ar_steps > 0:
+        def ar_step(seed):
+            return ctx.hbsjd_rollout(prefix, batch.prefix_len, batch.labels, batch.temperature,
+                                     1, top_k=wl.top_k, cfg_scale=wl.cfg_scale, seed=seed,
+                                     verify_mode=P.VERIFY_AR, max_rounds=max_rounds,
+                                     out_tokens=out_tokens, out_counts=out_counts)
+        ar_step(998)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for i in range(args.ar_steps):
+            ar_step(1000 + i)
+        torch.cuda.synchronize()
+        ar_elapsed = time.perf_counter() - t1
+        ar = {"ms_per_step": round(1000.0 * ar_elapsed / args.ar_steps, 3),
+              "steps": args.ar_steps}
+
     committed_per_step = int(np.sum(T - batch.prefix_len))
     value = committed_per_step * args.steps / elapsed
     counts_total = sum(int(r["verified"]) for r in results)    # committed tokens = sum of counts
@@ -224,6 +245,11 @@ def main() -> int:
     roof["launches"] = dom_n
     roof["avg_launch_us"] = round(1000.0 * dom_ms / max(dom_n, 1), 3)
     roof["time_share"] = round(t_s / elapsed, 4)
+
+    if ar is not None:
+        ar["value"] = round(committed_per_step * ar["steps"] * 1000.0 / (ar["ms_per_step"] * ar["steps"]), 1)
+        ar["unit"] = "tokens/s"
+        ar["speedup_of_sjd"] = round(value / ar["value"], 3)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -263,6 +289,7 @@ def main() -> int:
         "reject_rate": round(reject_rate, 4),
         "committed_tokens_per_step": committed_per_step,
         "roofline": roof,
+        "cached_ar": ar,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

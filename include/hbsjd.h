@@ -59,8 +59,16 @@ typedef enum hbsjd_exec_mode {
 } hbsjd_exec_mode;
 
 typedef enum hbsjd_verify_mode {
-    HBSJD_VERIFY_PROB = 0,   /* Sec. 4.2, Eq. 5 */
-    HBSJD_VERIFY_GREEDY = 1  /* Sec. 4.2, Eq. 4 */
+    HBSJD_VERIFY_PROB = 0,      /* Sec. 4.2, Eq. 5 */
+    HBSJD_VERIFY_GREEDY = 1,    /* Sec. 4.2, Eq. 4 */
+    /* The cached autoregressive baseline the paper compares against (Sec. 5,
+     * Tables 1-5): `window` and `history` are ignored; the prefill covers
+     * positions 0..k_b-1 and every round forwards one row per image (its last
+     * committed token, or the class token, at position n_b) and commits one
+     * token drawn from that row's distribution with u_draft(b, n_b + 1)
+     * (Eq. 1). Tokens equal those of HBSJD_VERIFY_PROB with W = 1. */
+    HBSJD_VERIFY_AR = 2,
+    HBSJD_VERIFY_AR_GREEDY = 3  /* the same, committing the argmax (lowest index on ties) */
 } hbsjd_verify_mode;
 
 /*
@@ -116,7 +124,7 @@ typedef struct hbsjd_rollout_args {
     const int32_t* prefix_len;      /* host [B]; k_b in [0, T]; image b generates T - k_b tokens */
     const int32_t* class_labels;    /* host [B]; in [0, n_classes) */
     const float* temperature;       /* host [B]; finite, > 0 */
-    int32_t window;                 /* W >= 1, Jacobi window (Sec. 4.2) */
+    int32_t window;                 /* W in [1, 64], Jacobi window (Sec. 4.2); ignored by the AR modes */
     int32_t history;                /* H >= 1, history offset of the draft fill (Sec. 4.2) */
     int32_t top_k;                  /* 0 = off; otherwise keep entries >= the k-th largest */
     float cfg_scale;                /* 0 = no guidance; else l_u + s (l_c - l_u) (Sec. 4.2) */

@@ -6,7 +6,8 @@ device memory and the stream. Importing this package does not load the
 library; the first call does, and raises if it has not been built.
 """
 from .binding import (  # noqa: F401
-    DTYPE_BF16, DTYPE_F32, KERNELS, EXEC_AUTO, EXEC_COMPACT, EXEC_FULL, VERIFY_GREEDY, VERIFY_PROB,
+    DTYPE_BF16, DTYPE_F32, KERNELS, EXEC_AUTO, EXEC_COMPACT, EXEC_FULL, VERIFY_AR, VERIFY_AR_GREEDY,
+    VERIFY_GREEDY, VERIFY_PROB,
     HbsjdError, Context, ModelDesc, hbsjd_philox, hbsjd_verify_probs, hbsjd_version,
     library_path, load_library,
 )

@@ -19,7 +19,7 @@ _lib = None
 
 DTYPE_F32, DTYPE_BF16 = 0, 1
 EXEC_AUTO, EXEC_FULL, EXEC_COMPACT = 0, 1, 2
-VERIFY_PROB, VERIFY_GREEDY = 0, 1
+VERIFY_PROB, VERIFY_GREEDY, VERIFY_AR, VERIFY_AR_GREEDY = 0, 1, 2, 3
 KERNELS = ["setup", "embed", "qkv", "attn", "oproj", "norm", "w13", "w2", "lmhead",
            "transform", "verify"]
 _STATUS = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EHIP", 4: "ESTATE", 5: "EINTERNAL"}

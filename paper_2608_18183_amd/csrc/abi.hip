@@ -84,6 +84,7 @@ struct hbsjd_ctx {
     // rollout state
     bool have_state = false;
     int B = 0, W = 0, Hh = 24, top_k = 0, cfg = 1, greedy = 0, exec_mode = 0, gamma = 0;
+    int ar = 0;   // cached-AR baseline rounds (W = 0: one row per image)
     int max_rounds = 0, max_pages = 0, rounds_launched = 0;
     float cfg_scale = 0.f;
     uint64_t seed = 0;
@@ -408,18 +409,19 @@ hbsjd_status check_device_error(hbsjd_ctx* c) {
 hbsjd_status validate_args(const hbsjd_ctx* c, const hbsjd_rollout_args* a) {
     if (!a) return fail(HBSJD_EINVAL, "args is NULL");
     if (a->batch < 1) return fail(HBSJD_EINVAL, "batch must be >= 1");
-    if (a->window < 1 || a->window > 64) return fail(HBSJD_EINVAL, "window must be in [1, 64]");
-    if (a->history < 1) return fail(HBSJD_EINVAL, "history must be >= 1");
+    if (a->verify_mode < HBSJD_VERIFY_PROB || a->verify_mode > HBSJD_VERIFY_AR_GREEDY)
+        return fail(HBSJD_EINVAL, "unknown verify_mode");
+    const bool ar = a->verify_mode >= HBSJD_VERIFY_AR;
+    if (!ar && (a->window < 1 || a->window > 64)) return fail(HBSJD_EINVAL, "window must be in [1, 64]");
+    if (!ar && a->history < 1) return fail(HBSJD_EINVAL, "history must be >= 1");
     if (a->top_k < 0) return fail(HBSJD_EINVAL, "top_k must be >= 0");
     if (!std::isfinite(a->cfg_scale)) return fail(HBSJD_EINVAL, "cfg_scale must be finite");
-    if (a->verify_mode != HBSJD_VERIFY_PROB && a->verify_mode != HBSJD_VERIFY_GREEDY)
-        return fail(HBSJD_EINVAL, "unknown verify_mode");
     if (a->exec_mode < HBSJD_EXEC_AUTO || a->exec_mode > HBSJD_EXEC_COMPACT)
         return fail(HBSJD_EINVAL, "unknown exec_mode");
     if (a->gamma < -1) return fail(HBSJD_EINVAL, "gamma must be >= -1");
     if (!a->prefix_tokens || !a->prefix_len || !a->class_labels || !a->temperature)
         return fail(HBSJD_EINVAL, "prefix_tokens, prefix_len, class_labels and temperature are required");
-    if (!c->bf16 && c->T + a->window + 1 > 1024)
+    if (!c->bf16 && c->T + (ar ? 0 : a->window) + 1 > 1024)
         return fail(HBSJD_EINVAL, "fp32 mode supports T + window + 1 <= 1024");
     int need = 0;
     for (int b = 0; b < a->batch; ++b) {
@@ -440,15 +442,17 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
     TRY(validate_args(c, a));
     hipStream_t s = c->stream;
-    const int B = a->batch, T = c->T, W = a->window;
+    const bool ar = a->verify_mode >= HBSJD_VERIFY_AR;
+    const int B = a->batch, T = c->T, W = ar ? 0 : a->window;
     c->have_state = false;
     c->B = B;
     c->W = W;
-    c->Hh = a->history;
+    c->ar = ar;
+    c->Hh = ar ? 1 : a->history;
     c->top_k = a->top_k;
     c->cfg = a->cfg_scale != 0.f ? 2 : 1;
     c->cfg_scale = a->cfg_scale;
-    c->greedy = a->verify_mode == HBSJD_VERIFY_GREEDY;
+    c->greedy = a->verify_mode == HBSJD_VERIFY_GREEDY || a->verify_mode == HBSJD_VERIFY_AR_GREEDY;
     c->exec_mode = a->exec_mode;
     c->gamma = a->gamma >= 0 ? a->gamma : (c->gamma_cal >= 0 ? c->gamma_cal : B / 2);
     c->seed = a->seed;
@@ -462,17 +466,20 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     // prefill geometry (host knows the lengths)
     std::vector<int32_t> row0(1, 0), simg, sbr, lidx, pslots;
     int maxlen = 0;
+    // SJD prefills positions 0..k_b and drafts from the logits at k_b; the AR
+    // baseline prefills 0..k_b-1 and its first round forwards position k_b
     for (int b = 0; b < B; ++b) {
         const int k = a->prefix_len[b];
-        if (k >= T) continue;
+        const int pre = ar ? k : k + 1;
+        if (k >= T || pre == 0) continue;
         pslots.push_back(b);
         for (int br = 0; br < cfg; ++br) {
             simg.push_back(b);
             sbr.push_back(br);
-            lidx.push_back(row0.back() + k);
-            row0.push_back(row0.back() + k + 1);
+            lidx.push_back(row0.back() + pre - 1);
+            row0.push_back(row0.back() + pre);
         }
-        maxlen = std::max(maxlen, k + 1);
+        maxlen = std::max(maxlen, pre);
     }
     const int n_seq = (int)simg.size();
     const int pf_rows = row0.back();
@@ -588,6 +595,11 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
                         as<int32_t>(c->seg_pos0)},
                mp + kMetaSegs, n_seq, maxlen};
     forward_layers(c, fr);
+    if (ar) {   // the prefill only fills the cache
+        HIPTRY(c, hipGetLastError());
+        c->have_state = true;
+        return HBSJD_OK;
+    }
     // final norm of each sequence's last row, lm_head, transform, first window
     rmsnorm(c->bf16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, n_seq, c->g_out,
             c->m.rms_eps, c->d, c->hb.p, s);
@@ -650,7 +662,7 @@ void enqueue_round(hbsjd_ctx* c, int cur) {
                   as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
                   as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
-                  as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt};
+                  as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt, c->ar};
     {
         Timed tm(c, HBSJD_K_VERIFY);
         verify_commit(va, s);
@@ -661,6 +673,7 @@ void enqueue_round(hbsjd_ctx* c, int cur) {
 std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
     std::vector<uint64_t> g = {(uint64_t)c->B, (uint64_t)c->W, (uint64_t)c->cfg,
                                (uint64_t)c->Hh, (uint64_t)c->top_k, (uint64_t)c->greedy,
+                               (uint64_t)c->ar,
                                (uint64_t)c->max_rounds, (uint64_t)c->max_pages,
                                (uint64_t)c->kv_layer_elems};
     uint32_t cs;

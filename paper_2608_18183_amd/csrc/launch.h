@@ -168,6 +168,7 @@ struct VerifyArgs {
     int32_t* counts;         // [max_rounds][B] or null
     int64_t* stats;          // [4]
     int32_t* meta;
+    int ar = 0;              // cached-AR rounds: commit one draw of each image's single row
 };
 void verify_commit(const VerifyArgs& a, hipStream_t s);
 

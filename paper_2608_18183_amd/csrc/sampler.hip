@@ -365,6 +365,23 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     const int W = a.W, V = a.V, R = a.rows_per_slot;
     const int nC = (V + kChunk - 1) / kChunk;
     const uint64_t seed = meta_seed(a.meta);
+    if (a.ar) {
+        // cached AR: the image's single row predicts position n + 1 (Eq. 1)
+        if (t >= 64) return;
+        const int prow = sl * R;
+        const int z = a.greedy ? a.amax[prow]
+                               : wave_sample_cp(a.p + (size_t)prow * V, a.cprefix + (size_t)prow * (nC + 1),
+                                                V, nC, uniforms_at(seed, b, n + 1).draft);
+        if (t == 0) {
+            a.xtok[(size_t)b * a.T + n] = z;
+            const int round = a.meta[kMetaRound];
+            if (a.counts && round >= 0 && round < a.max_rounds) a.counts[(size_t)round * a.B + b] = 1;
+            atomicAdd((unsigned long long*)&a.stats[0], 1ull);
+            atomicAdd((unsigned long long*)&a.stats[2], 1ull);
+            a.cursor[b] = n + 1;
+        }
+        return;
+    }
     int n_new, base, nrows;
     if (a.prefill) {
         n_new = n;

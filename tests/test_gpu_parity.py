@@ -225,6 +225,72 @@ def test_rollout_bf16_full_equals_compact_and_counts_are_bounded():
     assert (t0 >= 0).all() and (t0 < shape.vocab).all()
 
 
+# ------------------------------------------------------------------ cached-AR baseline
+
+
+def _ar_counts_ok(counts, prefix_len, T):
+    """One token per round while an image is active, nothing after."""
+    for b, k in enumerate(prefix_len):
+        col = counts[:, b]
+        assert col.sum() == T - k
+        assert (col[:T - k] == 1).all() and (col[T - k:] == 0).all()
+
+
+@pytest.mark.parametrize("greedy,top_k", [(False, 0), (False, 20), (True, 0)])
+def test_rollout_ar_f32_tiny_equals_oracle_ar(tiny, greedy, top_k):
+    w, blob, om = tiny
+    batch = synth.make_batch(w, 3)
+    batch.prefix_len[1] = 0                 # the class token starts the sequence
+    batch.prefix_len[2] = w.model.T         # nothing to generate
+    batch.temperature[:] = [1.0, 0.6, 1.4, 1.9]
+    ctx = gu.make_ctx(w.model, "f32", blob)
+    g = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                          batch.temperature, 1, top_k=top_k, seed=321,
+                          verify_mode=P().VERIFY_AR_GREEDY if greedy else P().VERIFY_AR)
+    ref = om.rollout_ar(batch, top_k=top_k, seed=321, greedy=greedy)
+    assert np.array_equal(g["tokens"].cpu().numpy(), ref)
+    T = w.model.T
+    assert g["rounds"] == int(np.max(T - batch.prefix_len))
+    _ar_counts_ok(g["counts"].cpu().numpy(), batch.prefix_len, T)
+    assert g["rejected"] == 0
+
+
+def test_rollout_ar_f32_cfg_equals_oracle_ar():
+    shape = synth.small_shape(n_layers=2, d_model=32, n_heads=2, mlp_hidden=48, vocab=64,
+                              n_classes=4, grid=4)
+    blob = synth.make_weights(shape, 3, std=0.2)
+    om = oracle.Model(shape, blob)
+    w = synth.Workload("t", shape, "f32", 6, 3, 2, 7, 2.0, prefix_lo=0, prefix_hi=9)
+    batch = synth.make_batch(w, 5)
+    ctx = gu.make_ctx(shape, "f32", blob)
+    g = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                          batch.temperature, 1, top_k=7, cfg_scale=2.0, seed=78,
+                          verify_mode=P().VERIFY_AR)
+    ref = om.rollout_ar(batch, top_k=7, cfg_scale=2.0, seed=78)
+    assert np.array_equal(g["tokens"].cpu().numpy(), ref)
+
+
+def test_rollout_ar_bf16_equals_sjd_window_1():
+    # W = 1 SJD accepts every draft (its proposal is the same row recomputed),
+    # so it must reproduce the AR baseline token for token on the GPU as well
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 2, batch=4)
+    batch.prefix_len[:] = [shape.T - 40, 0, shape.T - 17, shape.T - 64]
+    ctx = gu.make_ctx(shape, "bf16", blob)
+    ar = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                           batch.temperature, 1, top_k=wl.top_k, seed=4242,
+                           verify_mode=P().VERIFY_AR)
+    sj = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                           batch.temperature, 1, top_k=wl.top_k, seed=4242)
+    a, s = ar["tokens"].cpu().numpy(), sj["tokens"].cpu().numpy()
+    assert np.array_equal(a, s)
+    assert sj["rejected"] == 0
+    _ar_counts_ok(ar["counts"].cpu().numpy(), batch.prefix_len, shape.T)
+    assert (a >= 0).all() and (a < shape.vocab).all()
+
+
 # ------------------------------------------------------------------ round API and errors
 
 
