@@ -166,6 +166,9 @@ def main() -> int:
     out_tokens = torch.empty((B, T), dtype=torch.int32, device="cuda")
     out_counts = torch.empty((max_rounds, B), dtype=torch.int32, device="cuda")
     mode = {"auto": P.EXEC_AUTO, "full": P.EXEC_FULL, "compact": P.EXEC_COMPACT}[args.exec_mode]
+    # the Full/Compact threshold from the library's latency test (Sec. 4.3),
+    # unless one is given; rollouts below pass gamma = -1 to use the context's
+    gamma = args.gamma if args.gamma >= 0 else ctx.hbsjd_calibrate_gamma(B, wl.window)
 
     def step(seed):
         return ctx.hbsjd_rollout(prefix, batch.prefix_len, batch.labels, batch.temperature,
@@ -283,7 +286,9 @@ def main() -> int:
                                f"{shape.grid}x{shape.grid}, batch {B}, W {wl.window}, "
                                f"top-k {wl.top_k}, cfg {wl.cfg_scale}",
                    "batch": B, "window": wl.window, "history": wl.history,
-                   "exec_mode": args.exec_mode, "parallelism": "single GPU"},
+                   "exec_mode": args.exec_mode, "gamma": gamma,
+                   "gamma_source": "given" if args.gamma >= 0 else "calibrated",
+                   "parallelism": "single GPU"},
         "mean_accepted_tokens_per_round": round(mean_accepted, 4),
         "rounds_per_step": rounds,
         "reject_rate": round(reject_rate, 4),

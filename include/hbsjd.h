@@ -216,11 +216,16 @@ hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t
                           void* stream);
 
 /*
- * Hardware calibration of the Full/Compact threshold (Sec. 4.3): times the
- * verifier round at several active counts A <= batch in both modes on
- * synthetic state and returns the largest A at which Compact is faster (the
- * context keeps it for gamma = -1). Needs loaded weights; outputs do not
- * depend on gamma.
+ * Hardware calibration of the Full/Compact threshold (Sec. 4.3, Eq. 6): a
+ * data-independent latency test. On synthetic state (`batch` images halfway
+ * through an all-zero prefix of class 0, window `window`, no guidance) it
+ * times the verifier forward in Full and in Compact mode with A = 1, 2, 4, ...,
+ * batch images active, and returns the largest A at which Compact is no
+ * slower. The context keeps it as the gamma of rollouts that pass gamma = -1.
+ * Rollout outputs never depend on gamma. Needs loaded weights; clears any
+ * round-API state (a following hbsjd_round returns HBSJD_ESTATE). Errors:
+ * EINVAL (batch < 1, window outside [1, 64], gamma NULL), ESTATE (no
+ * weights), ENOMEM, EHIP.
  */
 hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* ctx, int32_t batch, int32_t window,
                                    int32_t* gamma);

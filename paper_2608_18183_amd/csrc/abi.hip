@@ -78,6 +78,7 @@ struct hbsjd_ctx {
     DevBuf P[2], CP[2], amax[2], logits;
     DevBuf seq_row0, seq_img, seq_branch, lm_idx;
     DevBuf ptab, kv;
+    DevBuf calib_tok;   // all-zero prefixes of the gamma calibration
     int32_t* pin = nullptr;    // pinned host words: active counts of the last two rounds
     hipEvent_t ev[2] = {nullptr, nullptr};
 
@@ -162,7 +163,7 @@ hbsjd_ctx::~hbsjd_ctx() {
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
                      &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
                      &CP[0], &CP[1], &amax[0], &amax[1], &logits, &seq_row0, &seq_img,
-                     &seq_branch, &lm_idx, &ptab, &kv};
+                     &seq_branch, &lm_idx, &ptab, &kv, &calib_tok};
     for (DevBuf* b : all) free_buf(*b);
     if (pin) (void)hipHostFree(pin);
     for (auto& e : ev)
@@ -622,7 +623,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
 
 // queue the launches of one round on buffer parity `cur`; every launch sizes
 // itself from the device counts the round's set-up kernel writes
-void enqueue_round(hbsjd_ctx* c, int cur) {
+void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
     hipStream_t s = c->stream;
     const int B = c->B, W = c->W, cfg = c->cfg, S = B * cfg, R = W + 1;
     int32_t* mt = as<int32_t>(c->meta);
@@ -658,6 +659,7 @@ void enqueue_round(hbsjd_ctx* c, int cur) {
         Timed tm(c, HBSJD_K_TRANSFORM);
         transform(ta, s);
     }
+    if (!with_verify) return;
     VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds,
                   as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
                   as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
@@ -1178,12 +1180,72 @@ hbsjd_status hbsjd_profile_read(hbsjd_ctx* c, double* total_ms, int64_t* launche
 }
 
 hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* c, int32_t batch, int32_t window, int32_t* gamma) {
-    (void)batch;
-    (void)window;
     try {
         GUARD(c);
         if (!gamma) return fail(HBSJD_EINVAL, "gamma is NULL");
-        return fail(HBSJD_ESTATE, "calibration is not built yet");
+        if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
+        if (batch < 1 || window < 1 || window > 64)
+            return fail(HBSJD_EINVAL, "need batch >= 1 and window in [1, 64]");
+        hipStream_t s = c->stream;
+        const int B = batch, T = c->T, k = T / 2;
+        // data-independent state: every image halfway through an all-zero
+        // prefix of class 0; only the verifier forward is timed
+        TRY(ensure(c, c->calib_tok, (size_t)B * T * 4));
+        HIPTRY(c, hipMemsetAsync(c->calib_tok.p, 0, (size_t)B * T * 4, s));
+        std::vector<int32_t> plen(B, k), lab(B, 0), cur(B);
+        std::vector<float> tau(B, 1.f);
+        hbsjd_rollout_args a{};
+        a.batch = B;
+        a.prefix_tokens = as<int32_t>(c->calib_tok);
+        a.prefix_len = plen.data();
+        a.class_labels = lab.data();
+        a.temperature = tau.data();
+        a.window = window;
+        a.history = 24;
+        a.verify_mode = HBSJD_VERIFY_PROB;
+        a.exec_mode = HBSJD_EXEC_FULL;
+        a.gamma = 0;
+        a.max_rounds = T;
+        TRY(begin(c, &a, nullptr));
+        c->have_state = false;   // the synthetic state is not a rollout
+        hipEvent_t e0, e1;
+        HIPTRY(c, hipEventCreate(&e0));
+        HIPTRY(c, hipEventCreate(&e1));
+        auto time_mode = [&](int exec, float* us) -> hbsjd_status {
+            int32_t hdr[2] = {-1, exec};   // round index, exec mode
+            HIPTRY(c, hipMemcpyAsync(as<int32_t>(c->meta) + kMetaRound, &hdr[0], 4, hipMemcpyHostToDevice, s));
+            HIPTRY(c, hipMemcpyAsync(as<int32_t>(c->meta) + kMetaExec, &hdr[1], 4, hipMemcpyHostToDevice, s));
+            enqueue_round(c, 0, false);   // warm-up
+            constexpr int kReps = 3;
+            HIPTRY(c, hipEventRecord(e0, s));
+            for (int r = 0; r < kReps; ++r) enqueue_round(c, r & 1, false);
+            HIPTRY(c, hipEventRecord(e1, s));
+            HIPTRY(c, hipEventSynchronize(e1));
+            float ms = 0.f;
+            HIPTRY(c, hipEventElapsedTime(&ms, e0, e1));
+            *us = 1000.f * ms / kReps;
+            return HBSJD_OK;
+        };
+        int best = 0;
+        std::vector<int> cand;
+        for (int A = 1; A < B; A *= 2) cand.push_back(A);
+        cand.push_back(B);
+        hbsjd_status st = HBSJD_OK;
+        for (int A : cand) {
+            for (int b = 0; b < B; ++b) cur[b] = b < A ? k : T;
+            HIPTRY(c, hipMemcpyAsync(c->cursor.p, cur.data(), B * 4, hipMemcpyHostToDevice, s));
+            float t_full = 0.f, t_compact = 0.f;
+            if ((st = time_mode(HBSJD_EXEC_FULL, &t_full)) != HBSJD_OK) break;
+            if ((st = time_mode(HBSJD_EXEC_COMPACT, &t_compact)) != HBSJD_OK) break;
+            if (t_compact <= t_full) best = A;   // Eq. 6: Compact iff A <= gamma
+        }
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+        TRY(st);
+        HIPTRY(c, hipGetLastError());
+        c->gamma_cal = best;
+        *gamma = best;
+        return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_calibrate_gamma");
     }

@@ -359,3 +359,32 @@ def test_argument_errors(tiny):
     with pytest.raises(E) as ei:
         small.hbsjd_rollout(dev, batch.prefix_len, batch.labels, batch.temperature, 4)
     assert ei.value.code == "ENOMEM"
+
+
+# ------------------------------------------------------------------ gamma calibration
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_calibrate_gamma_drives_auto_mode(tiny, dtype):
+    if dtype == "f32":
+        w, blob, _ = tiny
+        shape, B, W = w.model, 4, w.window
+    else:
+        wl = synth.WORKLOADS["llamagen_b"]
+        shape, B, W = wl.model, 8, wl.window
+        blob = synth.make_weights(shape, 0)
+        w = synth.Workload("b8", shape, "bf16", B, W, 24, 0, 0.0, prefix_lo=0, prefix_hi=128)
+    ctx = gu.make_ctx(shape, dtype, blob)
+    g = ctx.hbsjd_calibrate_gamma(B, W)
+    assert 0 <= g <= B
+    with pytest.raises(P().HbsjdError):
+        ctx.hbsjd_round()                    # the synthetic state is not a rollout
+    batch = synth.make_batch(w, 9, batch=B)
+    batch.prefix_len[0] = shape.T - 2        # finishes early, so A shrinks
+    out = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                            batch.temperature, W, seed=5, exec_mode=P().EXEC_AUTO, gamma=-1)
+    for a, m in zip(out["active"], out["mode"]):
+        assert m == (0 if a > g else 1)      # Eq. 6 with the calibrated threshold
+    ref = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                            batch.temperature, W, seed=5, exec_mode=P().EXEC_FULL)
+    assert np.array_equal(out["tokens"].cpu().numpy(), ref["tokens"].cpu().numpy())
