@@ -75,7 +75,7 @@ struct hbsjd_ctx {
     DevBuf seg_seq, seg_row0, seg_nrows, seg_pos0;
     DevBuf slot_img, active_list, pf_slots;
     DevBuf h, hb, qb, ob, act, part;
-    DevBuf P[2], CP[2], amax[2], logits;
+    DevBuf P[2], CP[2], amax[2], samp, logits;
     DevBuf seq_row0, seq_img, seq_branch, lm_idx;
     DevBuf ptab, kv;
     DevBuf calib_tok;   // all-zero prefixes of the gamma calibration
@@ -162,7 +162,7 @@ hbsjd_ctx::~hbsjd_ctx() {
                      &meta, &meta_pf, &a_hist, &mode_hist, &stats, &counts_own, &row_tok,
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
                      &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
-                     &CP[0], &CP[1], &amax[0], &amax[1], &logits, &seq_row0, &seq_img,
+                     &CP[0], &CP[1], &amax[0], &amax[1], &samp, &logits, &seq_row0, &seq_img,
                      &seq_branch, &lm_idx, &ptab, &kv, &calib_tok};
     for (DevBuf* b : all) free_buf(*b);
     if (pin) (void)hipHostFree(pin);
@@ -517,6 +517,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
         TRY(ensure(c, c->CP[k], (size_t)out_rows * (c->nC + 1) * 4));
         TRY(ensure(c, c->amax[k], (size_t)out_rows * 4));
     }
+    TRY(ensure(c, c->samp, (size_t)out_rows * 4));
     if (cfg == 2) TRY(ensure(c, c->logits, (size_t)round_rows * c->V * 4));
     (void)counts_dev;
     TRY(ensure(c, c->counts_own, (size_t)a->max_rounds * B * 4));
@@ -607,12 +608,14 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     float* lg = cfg == 1 ? as<float>(c->P[1]) : as<float>(c->logits);
     gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, n_seq, lg, c->b_lm, s);
     TransformArgs ta{lg, as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
-                     as<int32_t>(c->pf_slots), as<float>(c->temps), 1, cfg, c->V, c->top_k,
-                     c->cfg_scale, mp + kMetaOutRows, (int)pslots.size(), as<int32_t>(c->meta)};
+                     as<int32_t>(c->samp), as<int32_t>(c->pf_slots), as<int32_t>(c->cursor),
+                     as<float>(c->temps), 1, cfg, c->V, c->top_k, T, c->cfg_scale,
+                     mp + kMetaOutRows, (int)pslots.size(), as<int32_t>(c->meta)};
     transform(ta, s);
     VerifyArgs va{B, W, T, c->Hh, c->V, c->greedy, 1, 1, c->max_rounds,
                   as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
-                  nullptr, as<int32_t>(c->pf_slots), mp + kMetaImgs, (int)pslots.size(),
+                  as<int32_t>(c->samp), nullptr, as<int32_t>(c->pf_slots), mp + kMetaImgs,
+                  (int)pslots.size(),
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
                   as<int32_t>(c->qsrc), nullptr, as<int64_t>(c->stats), as<int32_t>(c->meta)};
     verify_commit(va, s);
@@ -653,8 +656,9 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
                     c->b_lm, s);
     }
     TransformArgs ta{lg, as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
-                     as<int32_t>(c->slot_img), as<float>(c->temps), R, cfg, c->V, c->top_k,
-                     c->cfg_scale, mt + kMetaOutRows, B * R, mt};
+                     as<int32_t>(c->samp), as<int32_t>(c->slot_img), as<int32_t>(c->cursor),
+                     as<float>(c->temps), R, cfg, c->V, c->top_k, c->T, c->cfg_scale,
+                     mt + kMetaOutRows, B * R, mt};
     {
         Timed tm(c, HBSJD_K_TRANSFORM);
         transform(ta, s);
@@ -662,7 +666,8 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
     if (!with_verify) return;
     VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds,
                   as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
-                  as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img), mt + kMetaImgs, B,
+                  as<int32_t>(c->samp), as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img),
+                  mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
                   as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt, c->ar};
     {
@@ -687,7 +692,7 @@ std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
                       &c->seg_row0, &c->seg_nrows, &c->seg_pos0, &c->slot_img,
                       &c->active_list, &c->h, &c->hb, &c->qb, &c->ob, &c->act, &c->part,
                       &c->P[0], &c->P[1], &c->CP[0], &c->CP[1], &c->amax[0], &c->amax[1],
-                      &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope};
+                      &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope};
     for (DevBuf* b : bufs) g.push_back((uint64_t)(uintptr_t)b->p);
     return g;
 }

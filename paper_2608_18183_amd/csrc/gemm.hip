@@ -331,161 +331,6 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
         }
 }
 
-// ---------------------------------------------------------------- bf16, A resident
-// At the verifier's row counts (hundreds to a few thousand rows) the weights
-// are the large operand and each weight element serves few row tiles. Here a
-// workgroup keeps its 32 x Ks block of A in LDS for the whole K range (loaded
-// once, behind one barrier) and each wavefront streams its own 32 weight
-// columns from global memory straight into registers in the MFMA operand
-// layout, NSB 64-deep steps ahead. The K loop has no barrier and no LDS
-// writes. Workgroup tile 32 x 128: four wavefronts side by side in N, each
-// 32 x 32. K steps run in the same order as in k_gemm_bf16, so both kernels
-// give the same sums.
-template <int NSB, typename Epi>
-__global__ __launch_bounds__(256) void k_gemm_bf16_ares(const uint16_t* __restrict__ A, int lda,
-                                                        const uint16_t* __restrict__ W, int N,
-                                                        int K, const int* __restrict__ m_dev,
-                                                        int m_cap, int splits,
-                                                        float* __restrict__ part, Epi epi) {
-    constexpr int BM = 32, BN = 128, BK = 64, TM = 2, TN = 2;
-    constexpr int kMaxSteps = 16;   // Ks <= 1024: the block is at most 64 KB
-    extern __shared__ u32x4_t Asm[];   // [BM][Ks / 8] 16-byte chunks
-
-    const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
-    const int tiles_m = (m_cap + BM - 1) / BM;
-    const int total = tiles_m * (N / BN) * splits;
-    const int per_xcd = (total + 7) >> 3;
-    // the same XCD-contiguous tile order as k_gemm_bf16
-    const int lin = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
-    if (lin >= total) return;
-    const int tm = lin % tiles_m;
-    const int nz = lin / tiles_m;
-    const int z = nz % splits, tn = nz / splits;
-    const int m0 = tm * BM, n0 = tn * BN;
-    if (m0 >= M) return;
-    const int Ks = K / splits, kbase = z * Ks, nk = Ks / BK;
-    const int cpr = Ks / 8;   // chunks per row of the block
-    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    const int c16 = lane & 15, g = lane >> 4;
-    const int wn0 = n0 + wv * 32;     // this wavefront's first column
-    const int col0 = wn0 + c16;
-
-    epi.begin_tile(wn0);
-    typename Epi::Row rinfo[TM][4];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-            rinfo[i][v] = epi.row_info(min(m0 + i * 16 + 4 * g + v, M - 1));
-
-    // weight fragments of step kt: lane holds column c16 + 16 j, k = 8 g .. 8 g + 7
-    // of each 32-wide half kk of the step
-    const uint16_t* wp = W + (size_t)col0 * K + kbase + 8 * g;
-    u32x4_t B[NSB][TN][2];
-    auto bload = [&](u32x4_t (*b)[2], int kt) {
-        kt = kt < nk ? kt : nk - 1;
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk)
-                b[j][kk] = *reinterpret_cast<const u32x4_t*>(wp + (size_t)j * 16 * K + kt * BK + kk * 32);
-    };
-#pragma unroll
-    for (int s = 0; s < NSB - 1; ++s) bload(B[s], s);
-
-    // the A block: thread t moves chunks t, t + 256, ... (nk of them: the block
-    // has 32 * Ks / 8 = 256 * nk chunks); chunk q of row r sits at q ^ (r & 7)
-    {
-        u32x4_t ar[kMaxSteps];
-#pragma unroll
-        for (int i = 0; i < kMaxSteps; ++i)
-            if (i < nk) {
-                const int c = t + i * 256, r = c / cpr, q = c - r * cpr;
-                const int gm = min(m0 + r, M - 1);
-                ar[i] = *reinterpret_cast<const u32x4_t*>(A + (size_t)gm * lda + kbase + q * 8);
-            }
-#pragma unroll
-        for (int i = 0; i < kMaxSteps; ++i)
-            if (i < nk) {
-                const int c = t + i * 256, r = c / cpr, q = c - r * cpr;
-                Asm[r * cpr + (q ^ (r & 7))] = ar[i];
-            }
-    }
-    __syncthreads();
-
-    f32x4_t acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    auto step = [&](const u32x4_t (*b)[2], int kt) {
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            bf16x8_t af[TM];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const int r = i * 16 + c16;
-                const int q = kt * 8 + kk * 4 + g;
-                const u32x4_t v = Asm[r * cpr + (q ^ (r & 7))];
-                af[i] = __builtin_bit_cast(bf16x8_t, v);
-            }
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        af[i], __builtin_bit_cast(bf16x8_t, b[j][kk]), acc[i][j], 0, 0, 0);
-        }
-    };
-    // step kt uses stage kt % NSB; it first refills the stage step kt-1 used
-    const int nk_main = nk - nk % NSB;
-    for (int kt0 = 0; kt0 < nk_main; kt0 += NSB) {
-#pragma unroll
-        for (int s = 0; s < NSB; ++s) {
-            bload(B[(s + NSB - 1) % NSB], kt0 + s + NSB - 1);
-            step(B[s], kt0 + s);
-        }
-    }
-#pragma unroll
-    for (int s = 0; s < NSB - 1; ++s)
-        if (nk_main + s < nk) step(B[s], nk_main + s);
-
-    if (splits > 1) {
-        float* P = part + (size_t)z * m_cap * N;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int row = m0 + i * 16 + 4 * g + v;
-                if (row >= M) continue;
-#pragma unroll
-                for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
-            }
-        return;
-    }
-    typename Epi::Aux aux[TM][4][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = m0 + i * 16 + 4 * g + v;
-            const bool ok = row < M;
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const float val = acc[i][j][v];
-                const float partner = __shfl_xor(val, 1, 64);
-                if (ok) epi.store(rinfo[i][v], aux[i][v][j], row, col0 + j * 16, val, partner);
-            }
-        }
-}
-
 template <int BM, int BN, int WGM, int WGN, typename Epi>
 static void launch_bf16(const void* A, int lda, const void* W, int N, int K, const int* m_dev,
                         int m_cap, int splits, float* part, const Epi& epi, hipStream_t s) {

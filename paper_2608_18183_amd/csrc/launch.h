@@ -142,9 +142,11 @@ struct TransformArgs {
     float* p;                // distribution rows [out][V] (may equal logits without CFG)
     float* cprefix;          // [out][nchunks + 1]
     int32_t* amax;           // [out]
+    int32_t* samp;           // [out] each row's draw for the position it predicts (-1 past T)
     const int32_t* slot_img;
+    const int32_t* cursor;   // [B]: row i of image b predicts position cursor[b] + i + 1
     const float* temperature;   // [B]
-    int rows_per_slot, cfg, V, top_k;
+    int rows_per_slot, cfg, V, top_k, T;
     float cfg_scale;
     const int* nout_dev;
     int nout_cap;
@@ -157,6 +159,7 @@ struct VerifyArgs {
     const float* p;          // this round's distribution rows
     const float* cprefix;
     const int32_t* amax;
+    const int32_t* samp;     // this round's draft candidates (from the transform)
     const float* p_prev;     // previous round's rows (proposals)
     const int32_t* slot_img;
     const int* nimg_dev;

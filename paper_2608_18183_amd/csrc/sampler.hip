@@ -18,10 +18,87 @@ namespace hbsjd {
 constexpr int kBins = 1024;     // histogram bins of the top-k threshold search
 constexpr int kCand = 256;      // candidates ranked exactly once the bin is this small
 
+// ---------------------------------------------------------------- row staging
+// A 256-thread block holds one vocabulary row with thread t owning chunk t
+// (entries [64 t, 64 t + 64)) in registers: the layout every pinned chunk sum
+// needs. Global memory is read and written in whole 1 KB wavefront accesses and
+// transposed through LDS, half of a wavefront's chunks at a time: in half h,
+// stage[w][j] holds chunk 64 w + 32 h + j, padded to 68 floats so the owners'
+// 16-byte reads fall in distinct banks. Every thread of the block must call.
+constexpr int kStageStride = kChunk + 4;
+constexpr int kStageFloats = 4 * 32 * kStageStride;   // 34,816 bytes
+
+// op(k, x) receives entry 64 t + k of the calling thread for k = 0..63 (0 past
+// V; V is a multiple of 4)
+template <typename Op>
+__device__ __forceinline__ void stage_load_row(const float* __restrict__ row, int V, float* stage,
+                                               Op op) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    float* sw = stage + w * 32 * kStageStride;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int base = (64 * w + 32 * h) * kChunk;
+        float4 x[8];
+        // unconditional loads (entries past V re-read the row's last float4
+        // and are zeroed) so all eight stay in flight together
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int v = base + 256 * i + 4 * lane;
+            x[i] = *reinterpret_cast<const float4*>(row + (v < V ? v : V - 4));
+            if (v >= V) x[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = 256 * i + 4 * lane;
+            *reinterpret_cast<float4*>(sw + (e >> 6) * kStageStride + (e & 63)) = x[i];
+        }
+        __syncthreads();
+        if ((lane >> 5) == h) {
+            const float* mine = sw + (lane & 31) * kStageStride;
+#pragma unroll
+            for (int k = 0; k < kChunk; k += 4) {
+                const float4 y = *reinterpret_cast<const float4*>(mine + k);
+                op(k, y.x);
+                op(k + 1, y.y);
+                op(k + 2, y.z);
+                op(k + 3, y.w);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// writes row[0, V): val(k) gives entry 64 t + k of the calling thread
+template <typename Val>
+__device__ __forceinline__ void stage_store_row(float* __restrict__ row, int V, float* stage,
+                                                Val val) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    float* sw = stage + w * 32 * kStageStride;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int base = (64 * w + 32 * h) * kChunk;
+        if ((lane >> 5) == h) {
+            float* mine = sw + (lane & 31) * kStageStride;
+#pragma unroll
+            for (int k = 0; k < kChunk; k += 4)
+                *reinterpret_cast<float4*>(mine + k) = make_float4(val(k), val(k + 1), val(k + 2), val(k + 3));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = 256 * i + 4 * lane;
+            const int v = base + e;
+            const float4 x = *reinterpret_cast<const float4*>(sw + (e >> 6) * kStageStride + (e & 63));
+            if (v < V) *reinterpret_cast<float4*>(row + v) = x;
+        }
+        __syncthreads();
+    }
+}
+
 // ---------------------------------------------------------------- transform
 // One 256-thread block per distribution row; thread c owns vocabulary chunk c
 // (64 consecutive entries) in registers.
-__global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_transform(TransformArgs a) {
     __shared__ float red[4];
     __shared__ int ired[8];
     __shared__ int hist[kBins];
@@ -29,6 +106,7 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     __shared__ float cand[kCand];
     __shared__ int s_int[4];
     __shared__ float s_flt[4];
+    __shared__ __attribute__((aligned(16))) float stage[kStageFloats];
 
     const int r = blockIdx.x;
     if (r >= min(*a.nout_dev, a.nout_cap)) return;
@@ -43,33 +121,23 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
 
     // guided logits, temperature, max and argmax (of the guided logits)
     float y[kChunk];
+    stage_load_row(lc, V, stage, [&](int k, float x) { y[k] = x; });
+    if (lu) stage_load_row(lu, V, stage, [&](int k, float x) { y[k] = x + a.cfg_scale * (y[k] - x); });
     float lmax = -INFINITY, ymax = -INFINITY, ymin = INFINITY;
     int lidx = 0x7fffffff;
     int nan_seen = 0;
     const int v0 = t * kChunk;
 #pragma unroll
-    for (int k = 0; k < kChunk; k += 4) {
-        float4 c4 = make_float4(0.f, 0.f, 0.f, 0.f), u4 = c4;
-        const bool in = v0 + k < V;
-        if (in) {
-            c4 = *reinterpret_cast<const float4*>(lc + v0 + k);
-            if (lu) u4 = *reinterpret_cast<const float4*>(lu + v0 + k);
-        }
-        const float cv[4] = {c4.x, c4.y, c4.z, c4.w};
-        const float uv[4] = {u4.x, u4.y, u4.z, u4.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int v = v0 + k + q;
-            float l = cv[q];
-            if (lu) l = uv[q] + a.cfg_scale * (cv[q] - uv[q]);
-            const float yy = l / tau;
-            y[k + q] = yy;
-            if (v < V) {
-                if (l != l) nan_seen = 1;
-                if (l > lmax) { lmax = l; lidx = v; }
-                ymax = fmaxf(ymax, yy);
-                ymin = fminf(ymin, yy);
-            }
+    for (int k = 0; k < kChunk; ++k) {
+        const int v = v0 + k;
+        const float l = y[k];
+        const float yy = l / tau;
+        y[k] = yy;
+        if (v < V) {
+            if (l != l) nan_seen = 1;
+            if (l > lmax) { lmax = l; lidx = v; }
+            ymax = fmaxf(ymax, yy);
+            ymin = fminf(ymin, yy);
         }
     }
     if (nan_seen) atomicOr(&a.meta[kMetaError], (int)kErrNanLogit);
@@ -228,27 +296,71 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     float* prow = a.p + (size_t)r * V;
     float psum = 0.f;
 #pragma unroll
-    for (int k = 0; k < kChunk; k += 4) {
-        float pv[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            pv[q] = y[k + q] / z;
-            psum = psum + pv[q];
-        }
-        if (v0 + k < V) *reinterpret_cast<float4*>(prow + v0 + k) = make_float4(pv[0], pv[1], pv[2], pv[3]);
+    for (int k = 0; k < kChunk; ++k) {
+        y[k] = y[k] / z;
+        psum = psum + y[k];
     }
-    __syncthreads();
-    if (t < nC) tot[t] = psum;
+    stage_store_row(prow, V, stage, [&](int k) { return y[k]; });
+    // chunk prefix of p: tot[c] becomes the sum of chunks 0..c-1 (pinned order)
+    if (t < nC) tot[t + 1] = psum;
     __syncthreads();
     if (t == 0) {
-        float* cp = a.cprefix + (size_t)r * (nC + 1);
         float run = 0.f;
-        cp[0] = 0.f;
+        tot[0] = 0.f;
         for (int c = 0; c < nC; ++c) {
-            run = run + tot[c];
-            cp[c + 1] = run;
+            run = run + tot[c + 1];
+            tot[c + 1] = run;
         }
     }
+    __syncthreads();
+    float* cp = a.cprefix + (size_t)r * (nC + 1);
+    for (int c = t; c <= nC; c += 256) cp[c] = tot[c];
+
+    // draft candidate of this row: the position it predicts is n_b + i + 1 no
+    // matter how the round's verification ends, so its draw from p with
+    // u_draft(b, n_b + i + 1) is taken here, with the row's own prefix; the
+    // same search as wave_sample_cp, hence the same token
+    const int pos = min(a.cursor[b], a.T) + i + 1;
+    int z_draft = -1;
+    if (pos <= a.T) {
+        const float target = uniforms_at(meta_seed(a.meta), b, pos).draft * tot[nC];
+        if (t < 64) {
+            int cs = 0x7fffffff;
+            for (int c = t; c < nC; c += 64)
+                if (tot[c + 1] > target) { cs = c; break; }
+            cs = wave_min_int(cs);
+            if (t == 0) s_int[0] = cs;
+        }
+        __syncthreads();
+        const int cs = s_int[0];
+        __syncthreads();
+        if (cs == 0x7fffffff) {   // last positive entry of the row
+            int last = -1;
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k)
+                if (v0 + k < V && y[k] > 0.f) last = v0 + k;
+            last = wave_max_int(last);
+            if (t == 0) s_int[1] = -1;
+            __syncthreads();
+            if ((t & 63) == 0) atomicMax(&s_int[1], last);
+        } else if (t == cs) {
+            const float before = tot[cs];
+            float inner = 0.f;
+            int found = -1, lastpos = -1;
+#pragma unroll
+            for (int k = 0; k < kChunk; ++k) {
+                if (found < 0 && v0 + k < V) {
+                    inner = inner + y[k];
+                    if (y[k] > 0.f) lastpos = v0 + k;
+                    if (before + inner > target) found = v0 + k;
+                }
+            }
+            s_int[1] = found >= 0 ? found : lastpos;
+        }
+        __syncthreads();
+        z_draft = s_int[1];
+    }
+    if (t == 0) a.samp[r] = z_draft;
 }
 
 void transform(const TransformArgs& a, hipStream_t s) {
@@ -347,10 +459,75 @@ __device__ int block_inv_cdf(F w, int V, float u, float* cp, int* res) {
     return *res;
 }
 
+// Block-level draw from non-negative weights held chunk-owned in registers
+// (thread t has entries 64 t .. 64 t + 63 in w); the same association and the
+// same answer as block_inv_cdf. Returns -1 when every weight is zero. All 256
+// threads must call it.
+__device__ inline int block_inv_cdf_regs(const float (&w)[kChunk], int V, float u, float* cp,
+                                         int* res) {
+    const int t = threadIdx.x;
+    const int nC = (V + kChunk - 1) / kChunk;
+    const int v0 = t * kChunk;
+    float sum = 0.f;
+    int last = -1;
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k)
+        if (v0 + k < V) {
+            sum = sum + w[k];
+            if (w[k] > 0.f) last = v0 + k;
+        }
+    if (t < nC) cp[t + 1] = sum;
+    __syncthreads();
+    if (t == 0) {
+        float run = 0.f;
+        cp[0] = 0.f;
+        for (int c = 0; c < nC; ++c) {
+            run = run + cp[c + 1];
+            cp[c + 1] = run;
+        }
+    }
+    __syncthreads();
+    const float total = cp[nC];
+    if (!(total > 0.f)) return -1;
+    const float target = u * total;
+    if (t < 64) {
+        int cs = 0x7fffffff;
+        for (int c = t; c < nC; c += 64)
+            if (cp[c + 1] > target) { cs = c; break; }
+        cs = wave_min_int(cs);
+        if (t == 0) *res = cs;
+    }
+    __syncthreads();
+    const int cs = *res;
+    __syncthreads();
+    if (cs == 0x7fffffff) {   // rounding left the target above the total: last positive entry
+        const int lw = wave_max_int(last);
+        if (t == 0) *res = -1;
+        __syncthreads();
+        if ((t & 63) == 0) atomicMax(res, lw);
+    } else if (t == cs) {
+        const float before = cp[cs];
+        float inner = 0.f;
+        int found = -1, lastpos = -1;
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            if (found < 0 && v0 + k < V) {
+                inner = inner + w[k];
+                if (w[k] > 0.f) lastpos = v0 + k;
+                if (before + inner > target) found = v0 + k;
+            }
+        }
+        *res = found >= 0 ? found : lastpos;
+    }
+    __syncthreads();
+    return *res;
+}
+
 // ---------------------------------------------------------------- verify + commit + refresh
 // One 256-thread block per processed image.
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     __shared__ float cp[kMaxChunks + 1];
+    __shared__ __attribute__((aligned(16))) float stage[kStageFloats];
     __shared__ int s_res;
     __shared__ int s_first;
     __shared__ int old_dr[64], old_q[64];
@@ -369,9 +546,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
         // cached AR: the image's single row predicts position n + 1 (Eq. 1)
         if (t >= 64) return;
         const int prow = sl * R;
-        const int z = a.greedy ? a.amax[prow]
-                               : wave_sample_cp(a.p + (size_t)prow * V, a.cprefix + (size_t)prow * (nC + 1),
-                                                V, nC, uniforms_at(seed, b, n + 1).draft);
+        const int z = a.greedy ? a.amax[prow] : a.samp[prow];
         if (t == 0) {
             a.xtok[(size_t)b * a.T + n] = z;
             const int round = a.meta[kMetaRound];
@@ -425,15 +600,23 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
                 const float* pr = a.p + (size_t)prow * V;
                 const int qs = old_q[js - 1];
                 const int z = old_dr[js - 1];
-                const float* qr = qs >= 0 ? a.p_prev + (size_t)qs * V : nullptr;
                 const float u = uniforms_at(seed, b, n + js).res;
-                rep = block_inv_cdf(
-                    [=](int v) {
-                        const float qv = qr ? qr[v] : (v == z ? 1.0f : 0.0f);
-                        const float d = pr[v] - qv;
-                        return d > 0.f ? d : 0.f;
-                    },
-                    V, u, cp, &s_res);
+                // residual max(0, p - q) of the rejected position, chunk-owned
+                float w[kChunk];
+                stage_load_row(pr, V, stage, [&](int k, float x) { w[k] = x; });
+                if (qs >= 0) {
+                    stage_load_row(a.p_prev + (size_t)qs * V, V, stage, [&](int k, float x) {
+                        const float d = w[k] - x;
+                        w[k] = d > 0.f ? d : 0.f;
+                    });
+                } else {   // history draft: point-mass proposal on z
+#pragma unroll
+                    for (int k = 0; k < kChunk; ++k) {
+                        const float d = w[k] - (t * kChunk + k == z ? 1.0f : 0.0f);
+                        w[k] = d > 0.f ? d : 0.f;
+                    }
+                }
+                rep = block_inv_cdf_regs(w, V, u, cp, &s_res);
                 if (rep < 0) {
                     if (t < 64) {
                         const int got = wave_sample_cp(pr, a.cprefix + (size_t)prow * (nC + 1), V, nC, u);
@@ -472,28 +655,24 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     }
     const int span = min(W, a.T - n_new);
     const int reused = min(span, base + nrows - n_new);   // positions covered by this round's rows
-    const int lane = t & 63, wv = t >> 6;
-    for (int m = 1 + wv; m <= reused; m += 4) {
+    // reused predictions: the transform drew each row's candidate for the
+    // position it predicts (u_draft of that position), or took its argmax
+    for (int m = 1 + t; m <= reused; m += 256) {
         const int pos = n_new + m;
-        const int i = pos - base - 1;
-        const int prow = sl * R + i;
-        int z;
-        if (a.greedy)
-            z = a.amax[prow];
-        else
-            z = wave_sample_cp(a.p + (size_t)prow * V, a.cprefix + (size_t)prow * (nC + 1), V, nC,
-                               uniforms_at(seed, b, pos).draft);
-        if (lane == 0) {
-            new_dr[m - 1] = z;
-            new_q[m - 1] = prow;
-        }
+        const int prow = sl * R + (pos - base - 1);
+        new_dr[m - 1] = a.greedy ? a.amax[prow] : a.samp[prow];
+        new_q[m - 1] = prow;
     }
     __syncthreads();
     if (t == 0) {
         for (int m = reused + 1; m <= span; ++m) {
             const int pos = n_new + m;
             const int src = pos - a.H >= 1 ? pos - a.H : pos - 1;
-            new_dr[m - 1] = src <= n_new ? a.xtok[(size_t)b * a.T + src - 1] : new_dr[src - n_new - 1];
+            // both candidates are loaded from their own arrays and the value
+            // selected, so neither access goes through a generic pointer
+            const int from_x = a.xtok[(size_t)b * a.T + max(min(src, n_new) - 1, 0)];
+            const int from_w = new_dr[max(src - n_new - 1, 0)];
+            new_dr[m - 1] = src <= n_new ? from_x : from_w;
             new_q[m - 1] = -1;
         }
     }
