@@ -79,6 +79,7 @@ struct hbsjd_ctx {
     DevBuf seq_row0, seq_img, seq_branch, lm_idx;
     DevBuf ptab, kv;
     DevBuf calib_tok;   // all-zero prefixes of the gamma calibration
+    DevBuf seg_pages;   // [segment][max_pages] KV page of each tile (attention's page list)
     int32_t* pin = nullptr;    // pinned host words: active counts of the last two rounds
     hipEvent_t ev[2] = {nullptr, nullptr};
 
@@ -163,7 +164,7 @@ hbsjd_ctx::~hbsjd_ctx() {
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
                      &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
                      &CP[0], &CP[1], &amax[0], &amax[1], &samp, &logits, &seq_row0, &seq_img,
-                     &seq_branch, &lm_idx, &ptab, &kv, &calib_tok};
+                     &seq_branch, &lm_idx, &ptab, &kv, &calib_tok, &seg_pages};
     for (DevBuf* b : all) free_buf(*b);
     if (pin) (void)hipHostFree(pin);
     for (auto& e : ev)
@@ -489,6 +490,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
 
     TRY(ensure_acts(c, std::max<long>(pf_rows, round_rows)));
     TRY(ensure_kv(c, S, T + W + 1));
+    TRY(ensure(c, c->seg_pages, (size_t)std::max(S, n_seq) * c->max_pages * 4));
     TRY(ensure(c, c->xtok, (size_t)B * T * 4));
     TRY(ensure(c, c->cursor, B * 4));
     TRY(ensure(c, c->drafts, (size_t)B * W * 4));
@@ -574,6 +576,8 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, segrow0.data(), n_seq * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seq * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seq * 4, hipMemcpyHostToDevice, s));
+    seg_pages(as<int32_t>(c->seg_seq), n_seq, as<int32_t>(c->ptab), c->max_pages,
+              as<int32_t>(c->seg_pages), s);
     std::vector<int32_t> mpf(kMetaCount, 0);
     mpf[kMetaRows] = pf_rows;
     mpf[kMetaSegs] = n_seq;
@@ -594,7 +598,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
                        as<int32_t>(c->row_seq)},
                mp + kMetaRows, pf_rows,
                Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows),
-                        as<int32_t>(c->seg_pos0)},
+                        as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
                mp + kMetaSegs, n_seq, maxlen};
     forward_layers(c, fr);
     if (ar) {   // the prefill only fills the cache
@@ -636,7 +640,8 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
                       as<int32_t>(c->active_list), as<int32_t>(c->row_tok), as<int32_t>(c->row_pos),
                       as<int32_t>(c->row_kv), as<int32_t>(c->row_seq), as<int32_t>(c->seg_seq),
                       as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0),
-                      mt, as<int32_t>(c->a_hist), as<int32_t>(c->mode_hist)};
+                      mt, as<int32_t>(c->a_hist), as<int32_t>(c->mode_hist),
+                      as<int32_t>(c->seg_pages)};
     {
         Timed tm(c, HBSJD_K_SETUP);
         round_setup(sa, s);
@@ -646,7 +651,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
                        as<int32_t>(c->row_seq)},
                mt + kMetaRows, rows_cap,
                Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows),
-                        as<int32_t>(c->seg_pos0)},
+                        as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
                mt + kMetaSegs, S, R};
     forward_layers(c, fr);
     float* lg = cfg == 1 ? as<float>(c->P[cur]) : as<float>(c->logits);
@@ -692,7 +697,8 @@ std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
                       &c->seg_row0, &c->seg_nrows, &c->seg_pos0, &c->slot_img,
                       &c->active_list, &c->h, &c->hb, &c->qb, &c->ob, &c->act, &c->part,
                       &c->P[0], &c->P[1], &c->CP[0], &c->CP[1], &c->amax[0], &c->amax[1],
-                      &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope};
+                      &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope,
+                      &c->seg_pages};
     for (DevBuf* b : bufs) g.push_back((uint64_t)(uintptr_t)b->p);
     return g;
 }
@@ -1075,6 +1081,7 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         TRY(ensure(c, c->seg_row0, (n_seqs + 1) * 4));
         TRY(ensure(c, c->seg_nrows, n_seqs * 4));
         TRY(ensure(c, c->seg_pos0, n_seqs * 4));
+        TRY(ensure(c, c->seg_pages, (size_t)n_seqs * c->max_pages * 4));
         std::vector<int32_t> segn(n_seqs), segpos(n_seqs, 0), mz(kMetaCount, 0);
         for (int q = 0; q < n_seqs; ++q) segn[q] = row0[q + 1] - row0[q];
         HIPTRY(c, hipMemcpyAsync(c->meta.p, mz.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
@@ -1092,6 +1099,8 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, row0.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
         HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
         HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+        seg_pages(as<int32_t>(c->seg_seq), n_seqs, as<int32_t>(c->ptab), c->max_pages,
+                  as<int32_t>(c->seg_pages), s);
         std::vector<int32_t> mpf(kMetaCount, 0);
         mpf[kMetaRows] = rows;
         mpf[kMetaSegs] = n_seqs;
@@ -1108,7 +1117,7 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
                            as<int32_t>(c->row_seq)},
                    mp + kMetaRows, rows,
                    Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0),
-                            as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0)},
+                            as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
                    mp + kMetaSegs, n_seqs, maxlen};
         forward_layers(c, fr);
         gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaRows, rows, logits,

@@ -25,30 +25,36 @@ __device__ inline bf16x8_t load_bf16x8(const uint16_t* p) {
 template <int NMT>
 __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ qb,
                                                    uint16_t* __restrict__ ob, int d, int H,
-                                                   const uint16_t* __restrict__ kv,
-                                                   const int32_t* __restrict__ ptab, int maxp,
+                                                   const uint16_t* __restrict__ kv, int maxp,
                                                    Segments seg, const int* __restrict__ nseg_dev,
                                                    int qblocks) {
     constexpr int QR = NMT * 16;   // query rows per block
     const int sb = blockIdx.x, head = blockIdx.y;
     const int sg = sb / qblocks, qblk = sb - sg * qblocks;
-    if (sg >= *nseg_dev) return;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    // the segment's metadata, the count and this wavefront's first page are
+    // independent loads (the grid covers the segment capacity, and the page
+    // list is indexed by segment), so they are in flight together
+    const int nseg = *nseg_dev;
     const int nrows = seg.nrows[sg];
+    const int row0s = seg.row0[sg];
+    const int pos0 = seg.pos0[sg];
+    const int page_w = seg.pages[(size_t)sg * maxp + min(w, maxp - 1)];
+    if (sg >= nseg) return;
     const int q0 = qblk * QR;
     if (q0 >= nrows) return;
     const int nq = min(QR, nrows - q0);
-    const int row0 = seg.row0[sg] + q0;
-    const int posf = seg.pos0[sg] + q0;
+    const int row0 = row0s + q0;
+    const int posf = pos0 + q0;
     const int ntiles = (posf + nq - 1) / 64 + 1;
-    const int sq = seg.seq[sg];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int g = lane >> 4, c16 = lane & 15;
 
-    // LDS: waves 1..3 own 16 KB regions [0, 48 KB) for P then their partial O;
-    // wave 0 keeps P at [48 KB, 56 KB) and merges in registers.
-    __shared__ __attribute__((aligned(16))) float lds[14336];
+    // LDS: wavefront w owns region w (QR x 64 floats): P (bf16) during the tile
+    // loop, then its partial output for the merge
+    __shared__ __attribute__((aligned(16))) float lds[4 * QR * 64];
     __shared__ float mls[4][2][QR];
-    uint16_t* Pw = reinterpret_cast<uint16_t*>(w == 0 ? lds + 12288 : lds + (w - 1) * 4096);
+    float* Ow = lds + w * QR * 64;
+    uint16_t* Pw = reinterpret_cast<uint16_t*>(Ow);
 
     bf16x8_t qf[NMT][2];
 #pragma unroll
@@ -75,7 +81,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
 
     const size_t page_elems = (size_t)2 * H * 64 * 64;
     for (int tile = w; tile < ntiles; tile += 4) {
-        const int page = ptab[(size_t)sq * maxp + tile];
+        const int page = tile == w ? page_w : seg.pages[(size_t)sg * maxp + tile];
         const uint16_t* Kb = kv + (size_t)page * page_elems + (size_t)head * 4096;
         const uint16_t* Vb = kv + (size_t)page * page_elems + (size_t)(H + head) * 4096;
         // both operands of the tile are fetched before any MFMA so their
@@ -167,55 +173,46 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
                                                                        0, 0, 0);
             }
         }
-        // the next tile overwrites P: keep its writes after these reads
+        // the next tile (or the partial below) overwrites P: keep those writes
+        // after these reads
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    __syncthreads();
-    if (w > 0) {
-        float* Ow = lds + (w - 1) * 4096;
-#pragma unroll
-        for (int i = 0; i < NMT; ++i)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int r = i * 16 + 4 * g + v;
-#pragma unroll
-                for (int dj = 0; dj < 4; ++dj) Ow[r * 64 + dj * 16 + c16] = o[i][dj][v];
-                if (c16 == 0) {
-                    mls[w][0][r] = mrow[i][v];
-                    mls[w][1][r] = lrow[i][v];
-                }
-            }
-    }
-    __syncthreads();
-    if (w != 0) return;
-    // merge the four partials in wave order 0, 1, 2, 3
+    // every wavefront parks its partial (o, m, l); a wavefront without tiles
+    // parks m = -inf, l = 0
 #pragma unroll
     for (int i = 0; i < NMT; ++i)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int r = i * 16 + 4 * g + v;
-            if (r >= nq) continue;
-            float ms = mrow[i][v];
-            for (int ww = 1; ww < 4; ++ww) ms = fmaxf(ms, mls[ww][0][r]);
-            float sc[4];
-            sc[0] = __expf(mrow[i][v] - ms);
-            float l = sc[0] * lrow[i][v];
-            for (int ww = 1; ww < 4; ++ww) {
-                const float mw = mls[ww][0][r];
-                sc[ww] = mw == -INFINITY ? 0.f : __expf(mw - ms);
-                l += sc[ww] * mls[ww][1][r];
-            }
-            const float inv = 1.0f / l;
 #pragma unroll
-            for (int dj = 0; dj < 4; ++dj) {
-                const int dim = dj * 16 + c16;
-                float a = sc[0] * o[i][dj][v];
-                for (int ww = 1; ww < 4; ++ww) a += sc[ww] * lds[(ww - 1) * 4096 + r * 64 + dim];
-                ob[(size_t)(row0 + r) * d + head * 64 + dim] = f32_to_bf16(a * inv);
+            for (int dj = 0; dj < 4; ++dj) Ow[r * 64 + dj * 16 + c16] = o[i][dj][v];
+            if (c16 == 0) {
+                mls[w][0][r] = mrow[i][v];
+                mls[w][1][r] = lrow[i][v];
             }
         }
+    __syncthreads();
+    // merge the four partials in wave order 0, 1, 2, 3 (tile 0 is wave 0's, so
+    // its maximum is finite); wavefront w merges rows w, w + 4, ..., lane = dim
+    for (int r = w; r < nq; r += 4) {
+        const float m0 = mls[0][0][r];
+        float ms = m0;
+        for (int ww = 1; ww < 4; ++ww) ms = fmaxf(ms, mls[ww][0][r]);
+        float sc[4];
+        sc[0] = __expf(m0 - ms);
+        float l = sc[0] * mls[0][1][r];
+        for (int ww = 1; ww < 4; ++ww) {
+            const float mw = mls[ww][0][r];
+            sc[ww] = mw == -INFINITY ? 0.f : __expf(mw - ms);
+            l += sc[ww] * mls[ww][1][r];
+        }
+        const float inv = 1.0f / l;
+        float a = sc[0] * lds[r * 64 + lane];
+        for (int ww = 1; ww < 4; ++ww) a += sc[ww] * lds[ww * QR * 64 + r * 64 + lane];
+        ob[(size_t)(row0 + r) * d + head * 64 + lane] = f32_to_bf16(a * inv);
+    }
 }
 
 // fp32: one wavefront per (row, head); scores over keys 0..pos in LDS.
@@ -270,23 +267,14 @@ void attention(bool bf16, const void* q, void* o, int d, int heads, int head_dim
     if (bf16) {
         if (nseg_cap <= 0) return;
         if (max_rows_per_seg <= 16) {
-            launch(k_attn_bf16<1>, dim3(nseg_cap, heads), dim3(256), 0, s,
-                               (const uint16_t*)q, (uint16_t*)o, d, heads,
-                               (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
-        } else if (max_rows_per_seg <= 32) {
-            launch(k_attn_bf16<2>, dim3(nseg_cap, heads), dim3(256), 0, s,
-                               (const uint16_t*)q, (uint16_t*)o, d, heads,
-                               (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
-        } else if (max_rows_per_seg <= 48) {
-            launch(k_attn_bf16<3>, dim3(nseg_cap, heads), dim3(256), 0, s,
-                               (const uint16_t*)q, (uint16_t*)o, d, heads,
-                               (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev, 1);
+            launch(k_attn_bf16<1>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
+                   (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, 1);
         } else {
-            const int qblocks = (max_rows_per_seg + 63) / 64;
-            launch(k_attn_bf16<4>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
-                               (const uint16_t*)q, (uint16_t*)o, d, heads,
-                               (const uint16_t*)kv_layer, ptab, max_pages, seg, nseg_dev,
-                               qblocks);
+            // 32 query rows per block; long (prefill) segments split into several
+            const int qblocks = (max_rows_per_seg + 31) / 32;
+            launch(k_attn_bf16<2>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
+                   (const uint16_t*)q, (uint16_t*)o, d, heads, (const uint16_t*)kv_layer,
+                   max_pages, seg, nseg_dev, qblocks);
         }
     } else {
         if (nrows_cap <= 0) return;

@@ -49,7 +49,11 @@ struct Segments {
     const int32_t* row0;
     const int32_t* nrows;
     const int32_t* pos0;
+    const int32_t* pages;   // [segment][max_pages]: KV page of each 64-key tile of its sequence
 };
+// pages[q][j] = ptab[seq[q]][j] for the nseg segments (host-built segment lists)
+void seg_pages(const int32_t* seq, int nseg, const int32_t* ptab, int max_pages, int32_t* pages,
+               hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM
 // C[M x N] = A[M x K] . W[N x K]^T with a fused epilogue. M is read from
@@ -115,6 +119,7 @@ struct RoundSetupArgs {
     int32_t* meta;
     int32_t* a_hist;
     int32_t* mode_hist;
+    int32_t* seg_pages;
 };
 void round_setup(const RoundSetupArgs& a, hipStream_t s);
 

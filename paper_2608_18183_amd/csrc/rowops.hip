@@ -2,6 +2,8 @@
 // mode (Sec. 4.3, Eq. 6), verifier-row assembly (last committed token followed
 // by the draft window at per-image positions and KV slots, Sec. 4.2), prefill
 // rows, the embedding gather, and RMSNorm.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -78,10 +80,13 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
         const int b = a.slot_img[s];
         int n = a.cursor[b];
         n = n > a.T ? a.T : n;
-        a.seg_seq[q] = b * a.cfg + br;
+        const int seq = b * a.cfg + br;
+        a.seg_seq[q] = seq;
         a.seg_row0[q] = q * R;
         a.seg_nrows[q] = R;
         a.seg_pos0[q] = n;
+        for (int j = 0; j < a.max_pages; ++j)
+            a.seg_pages[(size_t)q * a.max_pages + j] = a.ptab[(size_t)seq * a.max_pages + j];
     }
     if (t == 0) {
         const int round = a.meta[kMetaRound] + 1;
@@ -103,6 +108,21 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
 
 void round_setup(const RoundSetupArgs& a, hipStream_t s) {
     launch(k_round_setup, dim3(1), dim3(1024), 0, s, a);
+}
+
+__global__ void k_seg_pages(const int32_t* seq, int nseg, const int32_t* ptab, int maxp,
+                            int32_t* pages) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= nseg * maxp) return;
+    const int q = i / maxp, j = i - q * maxp;
+    pages[i] = ptab[(size_t)seq[q] * maxp + j];
+}
+
+void seg_pages(const int32_t* seq, int nseg, const int32_t* ptab, int max_pages, int32_t* pages,
+               hipStream_t s) {
+    const int n = nseg * max_pages;
+    if (n <= 0) return;
+    launch(k_seg_pages, dim3((n + 255) / 256), dim3(256), 0, s, seq, nseg, ptab, max_pages, pages);
 }
 
 // ---------------------------------------------------------------- prefill rows
@@ -157,46 +177,103 @@ void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V
 
 constexpr int kMaxPer = 24;   // d <= 1536
 
-template <typename T>
-__device__ inline void norm_store(const float* x, int per, const float* __restrict__ g, float eps,
-                                  int d, T* __restrict__ out) {
+// Every global load of these kernels is unconditional (lanes past d re-read
+// entry d - 1 and zero it afterwards) and raw: a bf16 value converted inside a
+// guarded block makes the compiler wait for each load before the next one.
+template <int PER>
+__device__ inline void load_gain(const float* __restrict__ g, int d, float (&gv)[PER]) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) gv[k] = g[min(lane + 64 * k, d - 1)];
+}
+
+template <typename T, int PER>
+__device__ inline void norm_store(const float (&x)[PER], const float (&gv)[PER], float eps, int d,
+                                  T* __restrict__ out) {
     const int lane = threadIdx.x & 63;
     float ss = 0.f;
 #pragma unroll
-    for (int k = 0; k < kMaxPer; ++k)
-        if (k < per) ss = fmaf(x[k], x[k], ss);
+    for (int k = 0; k < PER; ++k) ss = fmaf(x[k], x[k], ss);
     ss = wave_sum(ss);
     const float r = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
-    for (int k = 0; k < kMaxPer; ++k) {
+    for (int k = 0; k < PER; ++k) {
         const int i = lane + 64 * k;
-        if (k < per && i < d) Elem<T>::store(out + i, (x[k] * r) * g[i]);
+        if (i < d) Elem<T>::store(out + i, (x[k] * r) * gv[k]);
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nrows_dev,
+template <typename T> struct Raw;
+template <> struct Raw<float> {
+    using type = float;
+    __device__ static float f32(float v) { return v; }
+};
+template <> struct Raw<uint16_t> {
+    using type = uint16_t;
+    __device__ static float f32(uint16_t v) { return bf16_to_f32(v); }
+};
+
+template <typename T, int PER>
+__global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nrows_dev, int cap,
                                                     const T* __restrict__ tok_emb,
                                                     const T* __restrict__ cls_emb,
                                                     const float* __restrict__ g, float eps, int d,
                                                     float* __restrict__ h, T* __restrict__ hb) {
     const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (r >= *nrows_dev) return;
+    if (r >= cap) return;
+    // the gain, the row count and the token are fetched together (tok[r] is
+    // allocated for every r below the capacity); only the gather waits
+    float gv[PER];
+    load_gain(g, d, gv);
+    const int nrows = *nrows_dev;
     const int tok = rows.tok[r];
+    if (r >= nrows) return;
     const T* e = tok >= 0 ? tok_emb + (size_t)tok * d : cls_emb + (size_t)(-(tok + 1)) * d;
+    typename Raw<T>::type raw[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) raw[k] = e[min(lane + 64 * k, d - 1)];
+    float x[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) x[k] = lane + 64 * k < d ? Raw<T>::f32(raw[k]) : 0.f;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = lane + 64 * k;
+        if (i < d) h[(size_t)r * d + i] = x[k];
+    }
+    norm_store<T, PER>(x, gv, eps, d, hb + (size_t)r * d);
+}
+
+template <typename T, int PER>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
+                                                 const int32_t* src_idx, const int* nrows_dev,
+                                                 int cap, const float* __restrict__ g, float eps,
+                                                 int d, T* __restrict__ hb) {
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (r >= cap) return;
+    float gv[PER];
+    load_gain(g, d, gv);
+    const int nrows = *nrows_dev;
+    const int src = src_idx ? src_idx[r] : r;   // fetched with the count (r is below the capacity)
+    if (r >= nrows) return;
+    float x[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) x[k] = h[(size_t)src * d + min(lane + 64 * k, d - 1)];
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+        if (lane + 64 * k >= d) x[k] = 0.f;
+    norm_store<T, PER>(x, gv, eps, d, hb + (size_t)r * d);
+}
+
+// the per-lane element count of a row of d (a multiple of 64 in bf16 mode)
+template <typename F>
+static void by_per(int d, F f) {
     const int per = (d + 63) / 64;
-    float x[kMaxPer];
-#pragma unroll
-    for (int k = 0; k < kMaxPer; ++k) {
-        const int i = lane + 64 * k;
-        x[k] = (k < per && i < d) ? Elem<T>::load(e + i) : 0.f;
-    }
-#pragma unroll
-    for (int k = 0; k < kMaxPer; ++k) {
-        const int i = lane + 64 * k;
-        if (k < per && i < d) h[(size_t)r * d + i] = x[k];
-    }
-    norm_store(x, per, g, eps, d, hb + (size_t)r * d);
+    if (per <= 1) f(std::integral_constant<int, 1>{});
+    else if (per <= 4) f(std::integral_constant<int, 4>{});
+    else if (per <= 12) f(std::integral_constant<int, 12>{});
+    else if (per <= 16) f(std::integral_constant<int, 16>{});
+    else if (per <= 20) f(std::integral_constant<int, 20>{});
+    else f(std::integral_constant<int, 24>{});
 }
 
 void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
@@ -204,42 +281,31 @@ void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_
                 float* h, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     const dim3 grid((nrows_cap + 3) / 4);
-    if (bf16)
-        launch(k_embed_norm<uint16_t>, grid, dim3(256), 0, s, rows, nrows_dev,
-               (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain, eps, d, h, (uint16_t*)hb);
-    else
-        launch(k_embed_norm<float>, grid, dim3(256), 0, s, rows, nrows_dev, (const float*)tok_emb,
-               (const float*)cls_emb, gain, eps, d, h, (float*)hb);
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
-                                                 const int32_t* src_idx, const int* nrows_dev,
-                                                 const float* __restrict__ g, float eps, int d,
-                                                 T* __restrict__ hb) {
-    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (r >= *nrows_dev) return;
-    const int src = src_idx ? src_idx[r] : r;
-    const int per = (d + 63) / 64;
-    float x[kMaxPer];
-#pragma unroll
-    for (int k = 0; k < kMaxPer; ++k) {
-        const int i = lane + 64 * k;
-        x[k] = (k < per && i < d) ? h[(size_t)src * d + i] : 0.f;
-    }
-    norm_store(x, per, g, eps, d, hb + (size_t)r * d);
+    by_per(d, [&](auto P) {
+        constexpr int PER = decltype(P)::value;
+        if (bf16)
+            launch(k_embed_norm<uint16_t, PER>, grid, dim3(256), 0, s, rows, nrows_dev, nrows_cap,
+                   (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain, eps, d, h,
+                   (uint16_t*)hb);
+        else
+            launch(k_embed_norm<float, PER>, grid, dim3(256), 0, s, rows, nrows_dev, nrows_cap,
+                   (const float*)tok_emb, (const float*)cls_emb, gain, eps, d, h, (float*)hb);
+    });
 }
 
 void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     const dim3 grid((nrows_cap + 3) / 4);
-    if (bf16)
-        launch(k_rmsnorm<uint16_t>, grid, dim3(256), 0, s, h, src_idx, nrows_dev, gain, eps, d,
-               (uint16_t*)hb);
-    else
-        launch(k_rmsnorm<float>, grid, dim3(256), 0, s, h, src_idx, nrows_dev, gain, eps, d,
-               (float*)hb);
+    by_per(d, [&](auto P) {
+        constexpr int PER = decltype(P)::value;
+        if (bf16)
+            launch(k_rmsnorm<uint16_t, PER>, grid, dim3(256), 0, s, h, src_idx, nrows_dev,
+                   nrows_cap, gain, eps, d, (uint16_t*)hb);
+        else
+            launch(k_rmsnorm<float, PER>, grid, dim3(256), 0, s, h, src_idx, nrows_dev,
+                   nrows_cap, gain, eps, d, (float*)hb);
+    });
 }
 
 template <typename T, int PER>
@@ -250,8 +316,11 @@ __global__ __launch_bounds__(256) void k_reduce_norm(const float* __restrict__ p
                                                      T* __restrict__ hb) {
     constexpr int kSplitMax = 4;
     const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (r >= min(*nrows_dev, m_cap)) return;
-    // one phase of loads: every split's partial, the residual and the gain
+    if (r >= m_cap) return;
+    // one phase of loads, issued with the row count: every split's partial,
+    // the residual and the gain (rows below m_cap are always allocated; rows
+    // at or past the count store nothing)
+    const int nrows = *nrows_dev;
     float pz[kSplitMax][PER], hv[PER], gv[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
@@ -263,6 +332,7 @@ __global__ __launch_bounds__(256) void k_reduce_norm(const float* __restrict__ p
         hv[k] = in ? h[(size_t)r * d + i] : 0.f;
         gv[k] = in ? g[i] : 0.f;
     }
+    if (r >= nrows) return;
     float x[PER];
     float ss = 0.f;
 #pragma unroll
@@ -310,6 +380,8 @@ static void reduce_norm_dispatch(const float* part, int splits, int m_cap, float
         reduce_norm_launch<T, 12>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
     else if (per <= 16)
         reduce_norm_launch<T, 16>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    else if (per <= 20)
+        reduce_norm_launch<T, 20>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
     else
         reduce_norm_launch<T, 24>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
 }

@@ -39,18 +39,22 @@ __device__ __forceinline__ void stage_load_row(const float* __restrict__ row, in
     for (int h = 0; h < 2; ++h) {
         const int base = (64 * w + 32 * h) * kChunk;
         float4 x[8];
-        // unconditional loads (entries past V re-read the row's last float4
-        // and are zeroed) so all eight stay in flight together
+        // unconditional loads (entries past V re-read the row's last float4)
+        // so all eight stay in flight together; the zeroing past V is a
+        // select taken once they have landed (overwriting a register whose
+        // load is still in flight would make the compiler wait for it)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int v = base + 256 * i + 4 * lane;
             x[i] = *reinterpret_cast<const float4*>(row + (v < V ? v : V - 4));
-            if (v >= V) x[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int e = 256 * i + 4 * lane;
-            *reinterpret_cast<float4*>(sw + (e >> 6) * kStageStride + (e & 63)) = x[i];
+            const bool in = base + e < V;
+            const float4 y = make_float4(in ? x[i].x : 0.f, in ? x[i].y : 0.f, in ? x[i].z : 0.f,
+                                         in ? x[i].w : 0.f);
+            *reinterpret_cast<float4*>(sw + (e >> 6) * kStageStride + (e & 63)) = y;
         }
         __syncthreads();
         if ((lane >> 5) == h) {
@@ -95,16 +99,26 @@ __device__ __forceinline__ void stage_store_row(float* __restrict__ row, int V, 
     }
 }
 
+// order-preserving map of a float to an int (and back), for exact LDS min/max
+__device__ inline int float_key(float f) {
+    const int i = __builtin_bit_cast(int, f);
+    return i >= 0 ? i : i ^ 0x7fffffff;
+}
+__device__ inline float key_float(int k) {
+    return __builtin_bit_cast(float, k >= 0 ? k : k ^ 0x7fffffff);
+}
+
 // ---------------------------------------------------------------- transform
 // One 256-thread block per distribution row; thread c owns vocabulary chunk c
 // (64 consecutive entries) in registers.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_transform(TransformArgs a) {
+__global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     __shared__ float red[4];
     __shared__ int ired[8];
     __shared__ int hist[kBins];
     __shared__ float tot[kMaxChunks + 1];
     __shared__ float cand[kCand];
     __shared__ int s_int[4];
+    __shared__ int s_mm[2];
     __shared__ float s_flt[4];
     __shared__ __attribute__((aligned(16))) float stage[kStageFloats];
 
@@ -209,6 +223,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 s_int[0] = -1;
                 s_int[1] = 0;
                 s_int[2] = 0;
+                s_mm[0] = 0x7fffffff;
+                s_mm[1] = (int)0x80000000;
             }
             __syncthreads();
             for (int q = 3; q >= 0; --q) {
@@ -229,6 +245,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 thr = lo;
                 break;
             }
+            // the bins are recomputed below with the same arithmetic from copies
+            // the compiler cannot see through, so it does not keep all 64 of
+            // this thread's bins alive across the scan
+            float lo_b = lo, scale_b = scale;
+            asm volatile("" : "+v"(lo_b), "+v"(scale_b));
             if (cnt <= kCand) {
                 if (t == 0) s_int[3] = 0;
                 __syncthreads();
@@ -236,7 +257,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 for (int k = 0; k < kChunk; ++k) {
                     const float yy = y[k];
                     if (v0 + k < V && yy >= lo && yy <= hi) {
-                        int bin = (int)((yy - lo) * scale);
+                        int bin = (int)((yy - lo_b) * scale_b);
                         bin = bin > kBins - 1 ? kBins - 1 : bin;
                         if (bin == bstar) cand[atomicAdd(&s_int[3], 1)] = yy;
                     }
@@ -256,21 +277,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 thr = s_flt[0];
                 break;
             }
-            // narrow to the values that fell into the chosen bin
-            float blo = INFINITY, bhi = -INFINITY;
+            // narrow to the values that fell into the chosen bin: their exact
+            // minimum and maximum, through LDS atomics on an order-preserving
+            // integer image of the float (a register min/max chain over the 64
+            // entries is turned into a tree that costs ~50 registers)
 #pragma unroll
             for (int k = 0; k < kChunk; ++k) {
                 const float yy = y[k];
                 if (v0 + k < V && yy >= lo && yy <= hi) {
-                    int bin = (int)((yy - lo) * scale);
+                    int bin = (int)((yy - lo_b) * scale_b);
                     bin = bin > kBins - 1 ? kBins - 1 : bin;
-                    if (bin == bstar) { blo = fminf(blo, yy); bhi = fmaxf(bhi, yy); }
+                    if (bin == bstar) {
+                        const int key = float_key(yy);
+                        atomicMin(&s_mm[0], key);
+                        atomicMax(&s_mm[1], key);
+                    }
                 }
             }
-            blo = block_reduce(blo, red, [](float p, float q) { return fminf(p, q); });
-            bhi = block_reduce(bhi, red, [](float p, float q) { return fmaxf(p, q); });
-            lo = blo;
-            hi = bhi;
+            __syncthreads();
+            lo = key_float(s_mm[0]);
+            hi = key_float(s_mm[1]);
+            __syncthreads();
             above = above_new;
             thr = lo;   // only reached if the loop runs out: keeps at least k entries
         }
@@ -290,19 +317,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         float z = 0.f;
         for (int c = 0; c < nC; ++c) z = z + tot[c];
         s_flt[1] = z;
+        s_int[2] = -1;   // the row's last positive entry, gathered below
     }
     __syncthreads();
     const float z = s_flt[1];
     float* prow = a.p + (size_t)r * V;
     float psum = 0.f;
+    uint64_t pos_mask = 0;   // entries past V are 0, so never positive
 #pragma unroll
     for (int k = 0; k < kChunk; ++k) {
         y[k] = y[k] / z;
         psum = psum + y[k];
+        pos_mask |= (uint64_t)(y[k] > 0.f) << k;
     }
+    // this thread's last positive entry (the fallback of the draw below)
+    const int last_pos = pos_mask ? v0 + 63 - __clzll((long long)pos_mask) : -1;
     stage_store_row(prow, V, stage, [&](int k) { return y[k]; });
     // chunk prefix of p: tot[c] becomes the sum of chunks 0..c-1 (pinned order)
     if (t < nC) tot[t + 1] = psum;
+    {
+        const int lw = wave_max_int(last_pos);
+        if ((t & 63) == 0) atomicMax(&s_int[2], lw);
+    }
     __syncthreads();
     if (t == 0) {
         float run = 0.f;
@@ -333,32 +369,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
         __syncthreads();
         const int cs = s_int[0];
-        __syncthreads();
-        if (cs == 0x7fffffff) {   // last positive entry of the row
-            int last = -1;
+        if (cs == 0x7fffffff) {   // rounding left the target above the total
+            z_draft = s_int[2];
+        } else {
+            // the owner parks its chunk; wavefront 0 scans it in order, lane k
+            // holding entry k (the same sums as wave_sample_cp)
+            if (t == cs) {
 #pragma unroll
-            for (int k = 0; k < kChunk; ++k)
-                if (v0 + k < V && y[k] > 0.f) last = v0 + k;
-            last = wave_max_int(last);
-            if (t == 0) s_int[1] = -1;
-            __syncthreads();
-            if ((t & 63) == 0) atomicMax(&s_int[1], last);
-        } else if (t == cs) {
-            const float before = tot[cs];
-            float inner = 0.f;
-            int found = -1, lastpos = -1;
-#pragma unroll
-            for (int k = 0; k < kChunk; ++k) {
-                if (found < 0 && v0 + k < V) {
-                    inner = inner + y[k];
-                    if (y[k] > 0.f) lastpos = v0 + k;
-                    if (before + inner > target) found = v0 + k;
-                }
+                for (int k = 0; k < kChunk; k += 4)
+                    *reinterpret_cast<float4*>(&cand[k]) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
             }
-            s_int[1] = found >= 0 ? found : lastpos;
+            __syncthreads();
+            if (t < 64) {
+                const float pv = cand[t];
+                const float before = tot[cs];
+                float inner = 0.f;
+                int found = -1, lastpos = -1;
+                for (int k = 0; k < kChunk; ++k) {
+                    const float x = __shfl(pv, k, 64);
+                    if (cs * kChunk + k >= V) break;
+                    inner = inner + x;
+                    if (x > 0.f) lastpos = cs * kChunk + k;
+                    if (before + inner > target) { found = cs * kChunk + k; break; }
+                }
+                if (t == 0) s_int[1] = found >= 0 ? found : lastpos;
+            }
+            __syncthreads();
+            z_draft = s_int[1];
         }
-        __syncthreads();
-        z_draft = s_int[1];
     }
     if (t == 0) a.samp[r] = z_draft;
 }
