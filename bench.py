@@ -107,6 +107,23 @@ def rollout_work(cls, shape, prefix_len, counts, W, cfg, esz=2):
     return tot_b, tot_f
 
 
+def measured_traffic(cls):
+    """HBM bytes per launch of a kernel class from the committed counter
+    summary (profiles/hbm_traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled
+    by a copy of known size), or None when there is none or the kernel's
+    source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        rec = json.load(open(path))[cls]
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(shape, blob_rounded, batch, wl, n_img, rounds):
     """The oracle on the host: the first n_img images of the same batch, prefill
     plus `rounds` verification rounds; committed tokens per second."""
@@ -243,7 +260,7 @@ def main() -> int:
         roof = {"bound": "hbm", "achieved": round(tb / t_s / 1e9, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dominant)
     roof["kernel"] = dominant
     roof["launches"] = dom_n
     roof["avg_launch_us"] = round(1000.0 * dom_ms / max(dom_n, 1), 3)
