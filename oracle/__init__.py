@@ -47,7 +47,7 @@ class _Args(ctypes.Structure):
                 ("H", ctypes.c_int), ("top_k", ctypes.c_int), ("cfg_scale", ctypes.c_float),
                 ("seed", ctypes.c_uint64), ("greedy", ctypes.c_int),
                 ("exec_mode", ctypes.c_int), ("gamma", ctypes.c_int),
-                ("max_rounds", ctypes.c_int)]
+                ("max_rounds", ctypes.c_int), ("sync", ctypes.c_int)]
 
 
 class _Out(ctypes.Structure):
@@ -155,7 +155,8 @@ class Model:
         lib().om_rope(self._h, _ptr(v), int(pos))
         return v
 
-    def _args(self, batch, W, H, top_k, cfg_scale, seed, greedy, exec_mode, gamma, max_rounds):
+    def _args(self, batch, W, H, top_k, cfg_scale, seed, greedy, exec_mode, gamma, max_rounds,
+              sync=False):
         self._keep = [np.ascontiguousarray(batch.prefix_tokens, dtype=np.int32),
                       np.ascontiguousarray(batch.prefix_len, dtype=np.int32),
                       np.ascontiguousarray(batch.labels, dtype=np.int32),
@@ -164,16 +165,20 @@ class Model:
         assert self._keep[0].shape == (B, self.T)
         return _Args(B, *[_ptr(a) for a in self._keep], int(W), int(H), int(top_k),
                      float(cfg_scale), int(seed), int(greedy), int(exec_mode), int(gamma),
-                     int(max_rounds))
+                     int(max_rounds), int(bool(sync)))
 
     def rollout(self, batch, W: int, H: int = 24, top_k: int = 0, cfg_scale: float = 0.0,
                 seed: int = 0, greedy: bool = False, exec_mode: int = 2, gamma: int = 0,
-                max_rounds: Optional[int] = None, allow_partial: bool = False) -> dict:
-        """Batched SJD rollout. exec_mode 0 Full, 1 Compact, 2 Auto (Full iff A > gamma)."""
+                max_rounds: Optional[int] = None, allow_partial: bool = False,
+                sync: bool = False) -> dict:
+        """Batched SJD rollout. exec_mode 0 Full, 1 Compact, 2 Auto (Full iff A > gamma).
+        sync=True runs the Batch-Synchronous SJD ablation (shared window
+        boundaries, Sec. 4.2 and Table 2) instead of independent progress."""
         B = len(batch.prefix_len)
         if max_rounds is None:
             max_rounds = int(self.T - np.min(batch.prefix_len)) + 1
-        a = self._args(batch, W, H, top_k, cfg_scale, seed, greedy, exec_mode, gamma, max_rounds)
+        a = self._args(batch, W, H, top_k, cfg_scale, seed, greedy, exec_mode, gamma, max_rounds,
+                       sync)
         tokens = np.zeros((B, self.T), dtype=np.int32)
         counts = np.zeros((max_rounds, B), dtype=np.int32)
         rounds = np.zeros(1, dtype=np.int32)

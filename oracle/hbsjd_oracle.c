@@ -29,7 +29,12 @@
  *    "Independent progress"); CFG branches share one state and verify on the
  *    fused guided logits (same paragraph);
  *  - Full vs Compact execution differ only in which rows are physically
- *    processed; the per-round choice is Full iff A > gamma  (Sec. 4.3, Eq. 6).
+ *    processed; the per-round choice is Full iff A > gamma  (Sec. 4.3, Eq. 6);
+ *  - the Batch-Synchronous SJD ablation (Sec. 4.2 "From Single-Sequence to
+ *    Batched SJD", Fig. 1a, Table 2): every image works through the same
+ *    sequence of Jacobi windows; an image that has committed its whole current
+ *    window waits until every active image has done so, and only then does the
+ *    batch move on to the next window.
  *
  * Where the paper is silent the oracle takes these readings: the decoder is a
  * LlamaGen-style pre-norm transformer (RMSNorm eps 1e-5, 2D RoPE on adjacent
@@ -44,7 +49,11 @@
  * (image, position, 0, 0) gives the draft, accept and resample uniforms; every
  * sum over the vocabulary is associated as sequential sums inside consecutive
  * 64-entry chunks, chunk totals then added sequentially; the inverse CDF returns
- * the first entry whose inclusive prefix exceeds u * total.
+ * the first entry whose inclusive prefix exceeds u * total. For the
+ * batch-synchronous ablation, window w of image b spans positions
+ * k_b + wW + 1 .. min(k_b + (w+1)W, T) (each image counts windows from its own
+ * prefix); an image waiting at the boundary still forwards its last committed
+ * token and re-draws its first draft from that row, committing nothing.
  */
 #include <math.h>
 #include <stdint.h>
@@ -532,6 +541,7 @@ typedef struct {
     int exec_mode;              /* 0 Full, 1 Compact, 2 Auto (Eq. 6) */
     int gamma;
     int max_rounds;
+    int sync;                   /* 0 = independent progress, 1 = batch-synchronous windows */
 } om_rollout_args;
 
 typedef struct {
@@ -545,6 +555,7 @@ typedef struct {
 
 typedef struct {
     int n, active, k;
+    int e;               /* batch-synchronous mode: end of the current window */
     int* x;              /* [T+1], x[1..n] committed */
     int* wz;             /* [W]: draft at position n + 1 + m */
     int* wmass;          /* [W]: 1 if its proposal is a point mass */
@@ -651,6 +662,7 @@ static void img_prefill(const om_model* o, const om_rollout_args* a, om_img* st,
     st->n = k;
     for (int t = 1; t <= k; ++t) st->x[t] = a->prefix_tokens[(size_t)b * T + t - 1];
     st->active = k < T;
+    st->e = k + a->W < T ? k + a->W : T;
     if (!st->active) return;
     const int ncfg = a->cfg_scale != 0.0f ? 2 : 1;
     /* positions 0..k-1 go through the cache only; position k gives the logits */
@@ -670,7 +682,15 @@ static void img_prefill(const om_model* o, const om_rollout_args* a, om_img* st,
 static int img_round(const om_model* o, const om_rollout_args* a, om_img* st, int b) {
     const int T = o->T, V = o->m.V, W = a->W;
     const int n = st->n;
-    const int We = W < T - n ? W : T - n;
+    const int lim = a->sync ? st->e : T;
+    const int We = W < lim - n ? W : lim - n;
+    if (We == 0) {
+        /* waiting at a shared window boundary: row 0 only, nothing verified */
+        const int last = n == 0 ? -1 : st->x[n];
+        window_forward(o, a, st, b, n, 1, &last, !a->greedy);
+        refresh_window(o, a, st, b, n, n, 1);
+        return 0;
+    }
     int* rt = (int*)malloc(sizeof(int) * (We + 1));
     rt[0] = n == 0 ? -1 : st->x[n];
     for (int i = 1; i <= We; ++i) rt[i] = st->wz[i - 1];
@@ -740,6 +760,14 @@ int om_rollout(const om_model* o, const om_rollout_args* a, om_rollout_out* out)
         for (int b = 0; b < B; ++b) A += st[b].active;
         if (A == 0) break;
         if (rounds >= a->max_rounds) { status = -2; break; }
+        if (a->sync) {
+            /* the batch moves to the next window once no active image has
+               drafts of the current one left to verify */
+            int pending = 0;
+            for (int b = 0; b < B; ++b) pending |= st[b].active && st[b].n < st[b].e;
+            if (!pending)
+                for (int b = 0; b < B; ++b) st[b].e = st[b].e + a->W < T ? st[b].e + a->W : T;
+        }
         const int full = a->exec_mode == 0 || (a->exec_mode == 2 && A > a->gamma);
         if (out->active_hist) out->active_hist[rounds] = A;
         if (out->mode_hist) out->mode_hist[rounds] = full ? 0 : 1;

@@ -101,6 +101,87 @@ def test_images_are_independent(tiny):
     assert np.array_equal(r1["counts"][:, :3].sum(0), r2["counts"][:, :3].sum(0))
 
 
+# ------------------------------------------------------------------ batch-synchronous windows
+
+
+def replay_sync_schedule(counts, prefix_len, T, W):
+    """Replays per-round counts against the shared-window rule (Sec. 4.2,
+    Fig. 1a): image b's window w ends at min(k_b + (w+1) W, T); the batch moves
+    to window w+1 only when every active image has reached the end of window w;
+    until then an image at its boundary commits nothing. Returns the final
+    cursors."""
+    n = np.asarray(prefix_len, dtype=np.int64).copy()
+    e = np.minimum(n + W, T)
+    for c in counts:
+        act = n < T
+        if not np.any(act & (n < e)):
+            e = np.minimum(e + W, T)
+        for b in range(len(n)):
+            if not act[b]:
+                assert c[b] == 0
+            elif n[b] < e[b]:
+                assert 1 <= c[b] <= min(W, e[b] - n[b]), (b, n[b], e[b], c[b])
+            else:
+                assert c[b] == 0, (b, n[b], e[b], c[b])
+        n += c
+    return n
+
+
+@pytest.mark.parametrize("W,H", [(1, 24), (3, 24), (4, 2), (16, 3)])
+def test_sync_greedy_equals_greedy_ar(tiny, W, H):
+    w, _, om = tiny
+    b = _batch(w, 2)
+    r = om.rollout(b, W=W, H=H, seed=5, greedy=True, sync=True)
+    ar = om.rollout_ar(b, seed=5, greedy=True)
+    assert np.array_equal(r["tokens"], ar)
+    assert np.array_equal(replay_sync_schedule(r["counts"], b.prefix_len, w.model.T, W),
+                          np.full(len(b.prefix_len), w.model.T))
+
+
+@pytest.mark.parametrize("seed", [1000, 1001])
+def test_sync_window_one_is_token_by_token_sampling(tiny, seed):
+    w, _, om = tiny
+    b = _batch(w)
+    r = om.rollout(b, W=1, seed=seed, sync=True)
+    assert np.array_equal(r["tokens"], om.rollout_ar(b, seed=seed))
+
+
+def test_sync_single_window_is_independent_progress(tiny):
+    """When one window spans every suffix (W >= T - k_b) no boundary falls
+    before T, so the synchronous schedule is the independent one."""
+    w, _, om = tiny
+    b = _batch(w, 7)
+    T = w.model.T
+    b.prefix_len[:] = np.maximum(b.prefix_len, T - 16)
+    ind = om.rollout(b, W=16, seed=31)
+    syn = om.rollout(b, W=16, seed=31, sync=True)
+    assert np.array_equal(ind["tokens"], syn["tokens"])
+    assert np.array_equal(ind["counts"], syn["counts"])
+
+
+@pytest.mark.parametrize("W", [2, 4, 9])
+def test_sync_schedule_full_compact_and_waiting(tiny, W):
+    w, _, om = tiny
+    b = _batch(w, 3)
+    b.prefix_len[1] = 60
+    T = w.model.T
+    runs = [om.rollout(b, W=W, seed=11, exec_mode=m, gamma=2, sync=True) for m in (0, 1, 2)]
+    for r in runs[1:]:
+        assert np.array_equal(r["tokens"], runs[0]["tokens"])
+        assert np.array_equal(r["counts"], runs[0]["counts"])
+    r = runs[0]
+    n = replay_sync_schedule(r["counts"], b.prefix_len, T, W)
+    assert np.array_equal(n, np.full(len(b.prefix_len), T))
+    for i in range(len(b.prefix_len)):
+        assert np.array_equal(r["tokens"][i, :b.prefix_len[i]], b.prefix_tokens[i, :b.prefix_len[i]])
+    assert r["rounds"] <= T - int(b.prefix_len.min())
+    assert (r["counts"] == 0).any()
+    assert r["image_rounds"] == int((r["counts"] > 0).sum())
+    ind = om.rollout(b, W=W, seed=11)
+    assert r["rounds"] >= max(int(np.ceil((T - k) / W)) for k in b.prefix_len)
+    assert ind["verified"] == r["verified"] == int((T - b.prefix_len).sum())
+
+
 # ------------------------------------------------------------------ chi-square
 
 
@@ -127,13 +208,13 @@ def _exact_joint(om, shape, cls, top_k, tau, cfg):
     return out / out.sum()
 
 
-def _chi2_pvalue(om, shape, W, H, top_k, tau, cfg, n=20000, seed=123):
+def _chi2_pvalue(om, shape, W, H, top_k, tau, cfg, n=20000, seed=123, sync=False):
     V, T = shape.vocab, shape.T
     cls = 1
     probs = _exact_joint(om, shape, cls, top_k, tau, cfg)
     b = synth.Batch(np.zeros((n, T), dtype=np.int32), np.zeros(n, dtype=np.int32),
                     np.full(n, cls, dtype=np.int32), np.full(n, tau, dtype=np.float32))
-    r = om.rollout(b, W=W, H=H, top_k=top_k, cfg_scale=cfg, seed=seed, exec_mode=1)
+    r = om.rollout(b, W=W, H=H, top_k=top_k, cfg_scale=cfg, seed=seed, exec_mode=1, sync=sync)
     idx = np.zeros(n, dtype=np.int64)
     for t in range(T):
         idx = idx * V + r["tokens"][:, t]
@@ -159,6 +240,20 @@ def test_sjd_suffix_distribution_matches_brute_force(W, H, top_k, tau, cfg):
     assert pv > 1e-3, pv
     # the rollout really speculated: some rounds committed more than one token
     assert r["counts"].max() > 1 and r["rejected"] > 0
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("W,H,top_k,tau,cfg", [(2, 24, 0, 1.0, 0.0), (3, 1, 2, 1.0, 0.0),
+                                                (2, 2, 0, 0.7, 2.0)])
+def test_sync_suffix_distribution_matches_brute_force(W, H, top_k, tau, cfg):
+    """Batch-synchronous windows change which drafts are verified when, not the
+    law of the output: 20000 images share every window boundary, so most of
+    them wait (and re-draw their first draft) at each boundary."""
+    shape, _, om = _tiny_peaky()
+    pv, r = _chi2_pvalue(om, shape, W, H, top_k, tau, cfg, sync=True)
+    assert pv > 1e-3, pv
+    assert r["counts"].max() > 1 and r["rejected"] > 0
+    assert (r["counts"] == 0).any()      # waiting image-rounds happened
 
 
 @pytest.mark.slow
