@@ -263,3 +263,47 @@ def verify_probs(p: np.ndarray, q: np.ndarray, drafts: np.ndarray, u_acc: np.nda
     lib().om_verify_probs(B, W, V, _ptr(p), _ptr(q), _ptr(dr), _ptr(ua), _ptr(ur),
                           _ptr(counts), _ptr(tokens))
     return counts, tokens
+
+
+# ---------------------------------------------------------------- teacher scoring (Eq. 3)
+
+
+def bikl(ls, lt) -> np.ndarray:
+    """Bidirectional KL of Sec. 3.1, Eq. 3: D(p, q) = KL(p||q)/2 + KL(q||p)/2, where
+    p and q are the softmax of the student and teacher logits rows (last axis).
+    Computed in float64: log-probabilities through an explicit log-sum-exp."""
+    ls = np.asarray(ls, dtype=np.float64)
+    lt = np.asarray(lt, dtype=np.float64)
+
+    def log_softmax(l):
+        m = np.max(l, axis=-1, keepdims=True)
+        return l - (m + np.log(np.sum(np.exp(l - m), axis=-1, keepdims=True)))
+
+    lp, lq = log_softmax(ls), log_softmax(lt)
+    p, q = np.exp(lp), np.exp(lq)
+    kl_pq = np.sum(p * (lp - lq), axis=-1)
+    kl_qp = np.sum(q * (lq - lp), axis=-1)
+    return 0.5 * kl_pq + 0.5 * kl_qp
+
+
+def score_bikl(student: Model, teacher: Model, tokens, prefix_len, labels):
+    """The distillation loss of Eq. 3 for completed sequences (Sec. 3.1): both
+    models see [class, x_1..x_{T-1}] teacher-forced; the logits row at position
+    t-1 is each model's distribution of x_t; per image the biKL is averaged over
+    the generated positions t = k_b+1..T. Returns (per_position [B][T] float64,
+    entry t-1 for position t and 0 for t <= k_b; loss [B], 0 for k_b = T)."""
+    tokens = np.asarray(tokens)
+    B, T = tokens.shape
+    per = np.zeros((B, T))
+    loss = np.zeros(B)
+    seqs = [tokens[b, :T - 1] for b in range(B)]
+    ls = student.forward_batch(labels, seqs)
+    lt = teacher.forward_batch(labels, seqs)
+    for b in range(B):
+        k = int(prefix_len[b])
+        if k >= T:
+            continue
+        d = bikl(ls[b][k:T], lt[b][k:T])
+        per[b, k:T] = d
+        loss[b] = float(np.mean(d))
+    return per, loss
