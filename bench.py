@@ -152,6 +152,9 @@ def main() -> int:
     ap.add_argument("--cpu-images", type=int, default=0, help="images in the CPU sample (0 = auto)")
     ap.add_argument("--ar-steps", type=int, default=2,
                     help="timed rollouts of the cached-AR baseline after the SJD ones (0 = skip)")
+    ap.add_argument("--ablation-steps", type=int, default=1,
+                    help="timed rollouts per execution ablation: Full, Compact, a gamma sweep "
+                         "and Batch-Synchronous SJD (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the rollout shards by image with no "
@@ -237,6 +240,50 @@ def main() -> int:
               "steps": args.ar_steps}
 
     committed_per_step = int(np.sum(T - batch.prefix_len))
+
+    # execution ablations on the same batch (Sec. 5: Table 2 compares cached
+    # AR, Batch-Synchronous SJD and independent progress with Full execution;
+    # Tables 3 and 8 and Fig. 2c compare Full, Compact and the hybrid switch
+    # over gamma). Each is timed after one untimed rollout of its own setting.
+    ablations = None
+    if args.ablation_steps > 0:
+        def abl(exec_mode, g, progress):
+            def run(seed):
+                return ctx.hbsjd_rollout(prefix, batch.prefix_len, batch.labels,
+                                         batch.temperature, wl.window, history=wl.history,
+                                         top_k=wl.top_k, cfg_scale=wl.cfg_scale, seed=seed,
+                                         exec_mode=exec_mode, gamma=g, max_rounds=max_rounds,
+                                         out_tokens=out_tokens, out_counts=out_counts,
+                                         progress=progress)
+            run(997)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            rs = [run(1000 + i) for i in range(args.ablation_steps)]
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t2) / args.ablation_steps
+            ir = sum(r["image_rounds"] for r in rs)
+            full_rounds = sum(int(np.sum(r["mode"] == 0)) for r in rs)
+            return {"ms_per_step": round(1000.0 * dt, 3),
+                    "value": round(committed_per_step / dt, 1),
+                    "rounds": [r["rounds"] for r in rs],
+                    "full_rounds": full_rounds,
+                    "mean_accepted_tokens_per_round":
+                        round(sum(r["verified"] for r in rs) / max(ir, 1), 4)}
+        ind = P.PROGRESS_INDEPENDENT
+        ablations = {
+            "independent_full": abl(P.EXEC_FULL, 0, ind),
+            "independent_compact": abl(P.EXEC_COMPACT, 0, ind),
+            "batch_synchronous_full": abl(P.EXEC_FULL, 0, P.PROGRESS_SYNC),
+            "batch_synchronous_compact": abl(P.EXEC_COMPACT, 0, P.PROGRESS_SYNC),
+            "gamma_sweep": {str(g): abl(P.EXEC_AUTO, g, ind)
+                            for g in sorted({0, B // 8, B // 4, B // 2, B})},
+        }
+        if ar is not None:
+            for k in ("independent_full", "independent_compact", "batch_synchronous_full",
+                      "batch_synchronous_compact"):
+                ablations[k]["speedup_vs_cached_ar"] = round(
+                    ar["ms_per_step"] / ablations[k]["ms_per_step"], 3)
+
     value = committed_per_step * args.steps / elapsed
     counts_total = sum(int(r["verified"]) for r in results)    # committed tokens = sum of counts
     image_rounds = sum(r["image_rounds"] for r in results)
@@ -312,6 +359,7 @@ def main() -> int:
         "committed_tokens_per_step": committed_per_step,
         "roofline": roof,
         "cached_ar": ar,
+        "ablations": ablations,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

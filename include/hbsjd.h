@@ -72,6 +72,24 @@ typedef enum hbsjd_verify_mode {
 } hbsjd_verify_mode;
 
 /*
+ * How images move through their windows (Sec. 4.2, "From Single-Sequence to
+ * Batched SJD"; Fig. 1; Table 2).
+ */
+typedef enum hbsjd_progress {
+    /* HB-SJD: every image keeps its own cursor and window and advances by its
+     * own accepted count each round */
+    HBSJD_PROGRESS_INDEPENDENT = 0,
+    /* The Batch-Synchronous SJD ablation: window w of image b ends at
+     * min(k_b + (w+1) W, T); an image never verifies past its window's end,
+     * and one that has reached it waits (its row 0 is still forwarded and its
+     * first draft re-drawn from it; it commits nothing and records count 0)
+     * until every active image has reached its own, after which the whole
+     * batch moves to window w+1. The output distribution is unchanged; the
+     * verification rounds grow. Ignored by the AR modes. */
+    HBSJD_PROGRESS_SYNC = 1
+} hbsjd_progress;
+
+/*
  * The student: a class-conditional LlamaGen-style decoder (Sec. 3.1, Eq. 1;
  * the paper's students are LlamaGen-B and -L). Pre-norm blocks of RMSNorm ->
  * QKV -> 2D RoPE -> causal attention -> O projection + residual -> RMSNorm ->
@@ -133,12 +151,14 @@ typedef struct hbsjd_rollout_args {
     int32_t exec_mode;              /* hbsjd_exec_mode */
     int32_t gamma;                  /* AUTO threshold; -1 = the context's calibrated value */
     int32_t max_rounds;             /* capacity of `counts`; >= max_b (T - k_b) */
+    int32_t progress;               /* hbsjd_progress; 0 = independent (HB-SJD) */
 } hbsjd_rollout_args;
 
 /* Results of one rollout; the caller allocates every array. */
 typedef struct hbsjd_rollout_out {
     int32_t* tokens;            /* device [B][T]: the prefix, then the generated suffix */
-    int32_t* counts;            /* device [max_rounds][B]: tokens committed per round, 0 if inactive */
+    int32_t* counts;            /* device [max_rounds][B]: tokens committed per round, 0 if
+                                   inactive (or waiting at a synchronous window boundary) */
     int32_t* rounds;            /* host [1]: verification rounds run */
     int32_t* active_per_round;  /* host [max_rounds] or NULL: A at the start of each round */
     int32_t* mode_per_round;    /* host [max_rounds] or NULL: 0 Full, 1 Compact */
@@ -191,6 +211,44 @@ hbsjd_status hbsjd_get_state(hbsjd_ctx* ctx, int32_t* tokens, int32_t* cursors, 
  */
 hbsjd_status hbsjd_forward(hbsjd_ctx* ctx, int32_t n_seqs, const int32_t* tokens,
                            const int32_t* lens, const int32_t* labels, float* logits);
+
+/*
+ * Teacher scoring of completed rollouts: the distillation loss of Sec. 3.1,
+ * Eq. 3 for one batch. `student` and `teacher` are two contexts on the same
+ * GPU with loaded weights, the same grid and the same vocabulary (their depth
+ * and width may differ). For every image b with k_b < T both models run a
+ * teacher-forced forward over [class, x_1 .. x_{T-1}]; with p_S and p_T the
+ * plain softmax of each model's conditional logits at position t-1 (no
+ * temperature, top-k or guidance), the per-position divergence is
+ *   D_biKL = KL(p_S || p_T) / 2 + KL(p_T || p_S) / 2
+ * for the generated positions t = k_b+1 .. T.
+ *   tokens        device [B][T]: the completed sequences (x_T is never read)
+ *   prefix_len    host [B]: k_b in [0, T]
+ *   class_labels  host [B]: in [0, min(student, teacher n_classes))
+ *   per_position  device [B][T], written: entry t-1 holds D_biKL at position t,
+ *                 0 for t <= k_b
+ *   loss          device [B], written: the mean of image b's entries over
+ *                 t = k_b+1 .. T (Eq. 3's inner average), 0 when k_b = T
+ * Blocking. The logits live in library-owned scratch of each context
+ * ((T - k_b) summed over images, times vocab, fp32). Replaces any rollout
+ * state of both contexts (as hbsjd_forward does). EINVAL for B < 1, NULL
+ * buffers, one context passed twice, mismatched grid or vocabulary, k_b or a
+ * label out of range, or a token of x_1 .. x_{T-1} outside [0, vocab); ESTATE
+ * without weights; ENOMEM; EHIP.
+ */
+hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
+                              const int32_t* tokens, const int32_t* prefix_len,
+                              const int32_t* class_labels, float* per_position, float* loss);
+
+/*
+ * The scoring kernel on caller-supplied rows, for testing: out[r] =
+ * D_biKL(softmax(logits_s[r]), softmax(logits_t[r])) (Sec. 3.1, Eq. 3). All
+ * pointers are device memory; logits_s and logits_t fp32 [rows][V], out fp32
+ * [rows]. V must be a multiple of 4 in [4, 16384]. `stream` may be NULL.
+ * Blocking. EINVAL for bad sizes or NULL buffers.
+ */
+hbsjd_status hbsjd_bikl_rows(const float* logits_s, const float* logits_t, int64_t rows,
+                             int32_t V, float* out, void* stream);
 
 /*
  * The verification kernel (Sec. 4.2, Eq. 5) on caller-supplied rows, for

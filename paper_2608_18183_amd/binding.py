@@ -20,6 +20,7 @@ _lib = None
 DTYPE_F32, DTYPE_BF16 = 0, 1
 EXEC_AUTO, EXEC_FULL, EXEC_COMPACT = 0, 1, 2
 VERIFY_PROB, VERIFY_GREEDY, VERIFY_AR, VERIFY_AR_GREEDY = 0, 1, 2, 3
+PROGRESS_INDEPENDENT, PROGRESS_SYNC = 0, 1
 KERNELS = ["setup", "embed", "qkv", "attn", "oproj", "norm", "w13", "w2", "lmhead",
            "transform", "verify"]
 _STATUS = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EHIP", 4: "ESTATE", 5: "EINTERNAL"}
@@ -45,7 +46,7 @@ class _RolloutArgs(ctypes.Structure):
     _fields_ = [("batch", _I32), ("prefix_tokens", _P), ("prefix_len", _P), ("class_labels", _P),
                 ("temperature", _P), ("window", _I32), ("history", _I32), ("top_k", _I32),
                 ("cfg_scale", ctypes.c_float), ("seed", ctypes.c_uint64), ("verify_mode", _I32),
-                ("exec_mode", _I32), ("gamma", _I32), ("max_rounds", _I32)]
+                ("exec_mode", _I32), ("gamma", _I32), ("max_rounds", _I32), ("progress", _I32)]
 
 
 class _RolloutOut(ctypes.Structure):
@@ -61,6 +62,8 @@ _SIGS = {
     "hbsjd_round": (_I32, [_P, _I32, _P, _P]),
     "hbsjd_get_state": (_I32, [_P, _P, _P, _P, _P]),
     "hbsjd_forward": (_I32, [_P, _I32, _P, _P, _P, _P]),
+    "hbsjd_score_bikl": (_I32, [_P, _P, _I32, _P, _P, _P, _P, _P]),
+    "hbsjd_bikl_rows": (_I32, [_P, _P, ctypes.c_int64, _I32, _P, _P]),
     "hbsjd_verify_probs": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
@@ -178,7 +181,8 @@ class Context:
                "hbsjd_load_weights")
 
     def _args(self, prefix_tokens, prefix_len, class_labels, temperature, window, history,
-              top_k, cfg_scale, seed, verify_mode, exec_mode, gamma, max_rounds):
+              top_k, cfg_scale, seed, verify_mode, exec_mode, gamma, max_rounds,
+              progress=PROGRESS_INDEPENDENT):
         pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
         lab = np.ascontiguousarray(class_labels, dtype=np.int32)
         tau = np.ascontiguousarray(temperature, dtype=np.float32)
@@ -189,18 +193,19 @@ class Context:
         self._keep = [pl, lab, tau, prefix_tokens]
         a = _RolloutArgs(B, _P(_dev_ptr(prefix_tokens)), _np_ptr(pl), _np_ptr(lab), _np_ptr(tau),
                          int(window), int(history), int(top_k), float(cfg_scale), int(seed),
-                         int(verify_mode), int(exec_mode), int(gamma), int(max_rounds))
+                         int(verify_mode), int(exec_mode), int(gamma), int(max_rounds),
+                         int(progress))
         return a, B, max_rounds
 
     def hbsjd_rollout(self, prefix_tokens, prefix_len, class_labels, temperature, window: int,
                       history: int = 24, top_k: int = 0, cfg_scale: float = 0.0, seed: int = 0,
                       verify_mode: int = VERIFY_PROB, exec_mode: int = EXEC_AUTO,
                       gamma: int = -1, max_rounds: Optional[int] = None, out_tokens=None,
-                      out_counts=None) -> dict:
+                      out_counts=None, progress: int = PROGRESS_INDEPENDENT) -> dict:
         import torch
         a, B, max_rounds = self._args(prefix_tokens, prefix_len, class_labels, temperature,
                                       window, history, top_k, cfg_scale, seed, verify_mode,
-                                      exec_mode, gamma, max_rounds)
+                                      exec_mode, gamma, max_rounds, progress)
         dev = prefix_tokens.device
         tokens = out_tokens if out_tokens is not None else torch.empty(
             (B, self.desc.T), dtype=torch.int32, device=dev)
@@ -222,10 +227,11 @@ class Context:
                             window: int, history: int = 24, top_k: int = 0,
                             cfg_scale: float = 0.0, seed: int = 0,
                             verify_mode: int = VERIFY_PROB, exec_mode: int = EXEC_AUTO,
-                            gamma: int = -1, max_rounds: Optional[int] = None):
+                            gamma: int = -1, max_rounds: Optional[int] = None,
+                            progress: int = PROGRESS_INDEPENDENT):
         a, B, _ = self._args(prefix_tokens, prefix_len, class_labels, temperature, window,
                              history, top_k, cfg_scale, seed, verify_mode, exec_mode, gamma,
-                             max_rounds)
+                             max_rounds, progress)
         self._B, self._W = B, int(window)
         _check(self._lib.hbsjd_rollout_begin(self._h, ctypes.byref(a)), "hbsjd_rollout_begin")
 
@@ -256,6 +262,21 @@ class Context:
         _check(self._lib.hbsjd_forward(self._h, ln.size, _P(_dev_ptr(tokens)), _np_ptr(ln),
                                        _np_ptr(lab), _P(_dev_ptr(out))), "hbsjd_forward")
         return out
+
+    def hbsjd_score_bikl(self, teacher: "Context", tokens, prefix_len, class_labels):
+        """Eq. 3 scoring of completed sequences with this context as the student.
+        tokens: int32 device tensor [B, T]. Returns (per_position [B, T],
+        loss [B]) fp32 device tensors."""
+        import torch
+        pl = np.ascontiguousarray(prefix_len, dtype=np.int32)
+        lab = np.ascontiguousarray(class_labels, dtype=np.int32)
+        B = pl.size
+        per = torch.empty((B, self.desc.T), dtype=torch.float32, device=tokens.device)
+        loss = torch.empty(B, dtype=torch.float32, device=tokens.device)
+        _check(self._lib.hbsjd_score_bikl(self._h, teacher._h, B, _P(_dev_ptr(tokens)),
+                                          _np_ptr(pl), _np_ptr(lab), _P(_dev_ptr(per)),
+                                          _P(_dev_ptr(loss))), "hbsjd_score_bikl")
+        return per, loss
 
     def hbsjd_profile_start(self, classes=()):
         mask = 0
@@ -289,6 +310,20 @@ def hbsjd_verify_probs(p, q, drafts, u_acc, u_res, stream=None):
                                 _P(_dev_ptr(tokens)), _P(_stream_handle(stream))),
            "hbsjd_verify_probs")
     return counts, tokens
+
+
+def hbsjd_bikl_rows(logits_s, logits_t, stream=None):
+    """logits_s, logits_t: fp32 device tensors [rows, V]. Returns the per-row
+    bidirectional KL of their softmaxes, fp32 device tensor [rows]."""
+    import torch
+    rows, V = logits_s.shape
+    if tuple(logits_t.shape) != (rows, V):
+        raise ValueError("logits_s and logits_t must have the same shape")
+    out = torch.empty(rows, dtype=torch.float32, device=logits_s.device)
+    L = load_library()
+    _check(L.hbsjd_bikl_rows(_P(_dev_ptr(logits_s)), _P(_dev_ptr(logits_t)), rows, V,
+                             _P(_dev_ptr(out)), _P(_stream_handle(stream))), "hbsjd_bikl_rows")
+    return out
 
 
 def hbsjd_philox(seed: int, bt, stream=None):

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(HERE, "libhbsjd.so")
-SOURCES = ["abi.hip", "gemm.hip", "attention.hip", "rowops.hip", "sampler.hip"]
+SOURCES = ["abi.hip", "gemm.hip", "attention.hip", "rowops.hip", "sampler.hip", "score.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions stay off (hardware notes)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

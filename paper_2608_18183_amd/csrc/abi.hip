@@ -80,6 +80,9 @@ struct hbsjd_ctx {
     DevBuf ptab, kv;
     DevBuf calib_tok;   // all-zero prefixes of the gamma calibration
     DevBuf seg_pages;   // [segment][max_pages] KV page of each tile (attention's page list)
+    DevBuf win_end;     // [B] end of each image's current window (batch-synchronous progress)
+    DevBuf score_logits, score_idx, score_k;   // teacher scoring: selected logits rows, their
+                                               // output slots, prefix lengths
     int32_t* pin = nullptr;    // pinned host words: active counts of the last two rounds
     hipEvent_t ev[2] = {nullptr, nullptr};
 
@@ -87,6 +90,8 @@ struct hbsjd_ctx {
     bool have_state = false;
     int B = 0, W = 0, Hh = 24, top_k = 0, cfg = 1, greedy = 0, exec_mode = 0, gamma = 0;
     int ar = 0;   // cached-AR baseline rounds (W = 0: one row per image)
+    int sync = 0; // batch-synchronous windows instead of independent progress
+    hipEvent_t ev_done = nullptr;   // teacher scoring: this context's forward has been queued
     int max_rounds = 0, max_pages = 0, rounds_launched = 0;
     float cfg_scale = 0.f;
     uint64_t seed = 0;
@@ -164,7 +169,8 @@ hbsjd_ctx::~hbsjd_ctx() {
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
                      &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
                      &CP[0], &CP[1], &amax[0], &amax[1], &samp, &logits, &seq_row0, &seq_img,
-                     &seq_branch, &lm_idx, &ptab, &kv, &calib_tok, &seg_pages};
+                     &seq_branch, &lm_idx, &ptab, &kv, &calib_tok, &seg_pages, &win_end,
+                     &score_logits, &score_idx, &score_k};
     for (DevBuf* b : all) free_buf(*b);
     if (pin) (void)hipHostFree(pin);
     for (auto& e : ev)
@@ -177,6 +183,7 @@ hbsjd_ctx::~hbsjd_ctx() {
     for (auto& g : gexec)
         if (g) (void)hipGraphExecDestroy(g);
     if (ev_user) (void)hipEventDestroy(ev_user);
+    if (ev_done) (void)hipEventDestroy(ev_done);
     if (stream) (void)hipStreamDestroy(stream);
 }
 
@@ -421,6 +428,8 @@ hbsjd_status validate_args(const hbsjd_ctx* c, const hbsjd_rollout_args* a) {
     if (a->exec_mode < HBSJD_EXEC_AUTO || a->exec_mode > HBSJD_EXEC_COMPACT)
         return fail(HBSJD_EINVAL, "unknown exec_mode");
     if (a->gamma < -1) return fail(HBSJD_EINVAL, "gamma must be >= -1");
+    if (a->progress != HBSJD_PROGRESS_INDEPENDENT && a->progress != HBSJD_PROGRESS_SYNC)
+        return fail(HBSJD_EINVAL, "unknown progress mode");
     if (!a->prefix_tokens || !a->prefix_len || !a->class_labels || !a->temperature)
         return fail(HBSJD_EINVAL, "prefix_tokens, prefix_len, class_labels and temperature are required");
     if (!c->bf16 && c->T + (ar ? 0 : a->window) + 1 > 1024)
@@ -450,6 +459,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     c->B = B;
     c->W = W;
     c->ar = ar;
+    c->sync = !ar && a->progress == HBSJD_PROGRESS_SYNC;
     c->Hh = ar ? 1 : a->history;
     c->top_k = a->top_k;
     c->cfg = a->cfg_scale != 0.f ? 2 : 1;
@@ -498,6 +508,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     TRY(ensure(c, c->labels, B * 4));
     TRY(ensure(c, c->temps, B * 4));
     TRY(ensure(c, c->plen, B * 4));
+    if (c->sync) TRY(ensure(c, c->win_end, B * 4));
     TRY(ensure(c, c->meta, kMetaCount * 4));
     TRY(ensure(c, c->meta_pf, kMetaCount * 4));
     TRY(ensure(c, c->a_hist, (size_t)(a->max_rounds + 1) * 4));
@@ -541,6 +552,12 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     HIPTRY(c, hipMemcpyAsync(c->xtok.p, a->prefix_tokens, (size_t)B * T * 4, hipMemcpyDeviceToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->cursor.p, a->prefix_len, B * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->plen.p, a->prefix_len, B * 4, hipMemcpyHostToDevice, s));
+    std::vector<int32_t> wend;   // first window of each image: positions k_b+1 .. min(k_b+W, T)
+    if (c->sync) {
+        wend.resize(B);
+        for (int b = 0; b < B; ++b) wend[b] = std::min(a->prefix_len[b] + W, T);
+        HIPTRY(c, hipMemcpyAsync(c->win_end.p, wend.data(), B * 4, hipMemcpyHostToDevice, s));
+    }
     HIPTRY(c, hipMemcpyAsync(c->labels.p, a->class_labels, B * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemcpyAsync(c->temps.p, a->temperature, B * 4, hipMemcpyHostToDevice, s));
     HIPTRY(c, hipMemsetAsync(c->drafts.p, 0xff, (size_t)B * W * 4, s));
@@ -641,7 +658,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
                       as<int32_t>(c->row_kv), as<int32_t>(c->row_seq), as<int32_t>(c->seg_seq),
                       as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0),
                       mt, as<int32_t>(c->a_hist), as<int32_t>(c->mode_hist),
-                      as<int32_t>(c->seg_pages)};
+                      as<int32_t>(c->seg_pages), c->sync ? as<int32_t>(c->win_end) : nullptr};
     {
         Timed tm(c, HBSJD_K_SETUP);
         round_setup(sa, s);
@@ -674,7 +691,8 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
                   as<int32_t>(c->samp), as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img),
                   mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
-                  as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt, c->ar};
+                  as<int32_t>(c->qsrc), c->counts, as<int64_t>(c->stats), mt, c->ar,
+                  c->sync ? as<int32_t>(c->win_end) : nullptr};
     {
         Timed tm(c, HBSJD_K_VERIFY);
         verify_commit(va, s);
@@ -685,7 +703,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
 std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
     std::vector<uint64_t> g = {(uint64_t)c->B, (uint64_t)c->W, (uint64_t)c->cfg,
                                (uint64_t)c->Hh, (uint64_t)c->top_k, (uint64_t)c->greedy,
-                               (uint64_t)c->ar,
+                               (uint64_t)c->ar, (uint64_t)c->sync,
                                (uint64_t)c->max_rounds, (uint64_t)c->max_pages,
                                (uint64_t)c->kv_layer_elems};
     uint32_t cs;
@@ -697,7 +715,7 @@ std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
                       &c->seg_row0, &c->seg_nrows, &c->seg_pos0, &c->slot_img,
                       &c->active_list, &c->h, &c->hb, &c->qb, &c->ob, &c->act, &c->part,
                       &c->P[0], &c->P[1], &c->CP[0], &c->CP[1], &c->amax[0], &c->amax[1],
-                      &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope,
+                      &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope, &c->win_end,
                       &c->seg_pages};
     for (DevBuf* b : bufs) g.push_back((uint64_t)(uintptr_t)b->p);
     return g;
@@ -735,6 +753,84 @@ hbsjd_status launch_round(hbsjd_ctx* c) {
         HIPTRY(c, hipGetLastError());
     }
     c->rounds_launched += 1;
+    return HBSJD_OK;
+}
+
+// Teacher-forced forward through every layer. Sequence q is image simg[q]:
+// [class labels[image], tokens[image][0 .. lens[q]-1]] at positions 0..lens[q],
+// rows row0[q] .. row0[q+1]-1; its KV pages are those of sequence `image`.
+// check_len[image] prefix tokens of each image are range-checked first. Leaves
+// the final residual stream in c->h, its normed rows in c->hb and the row
+// count in meta_pf. Synchronous up to the layers' launches.
+hbsjd_status forward_core(hbsjd_ctx* c, int n_images, const int32_t* tokens,
+                          const std::vector<int32_t>& labels, const std::vector<int32_t>& check_len,
+                          const std::vector<int32_t>& simg, const std::vector<int32_t>& lens,
+                          std::vector<int32_t>& row0) {
+    const int n_seqs = (int)simg.size();
+    row0.assign(1, 0);
+    int maxlen = 0;
+    for (int q = 0; q < n_seqs; ++q) {
+        row0.push_back(row0.back() + lens[q] + 1);
+        maxlen = std::max(maxlen, lens[q] + 1);
+    }
+    hipStream_t s = c->stream;
+    const int rows = row0.back();
+    c->have_state = false;
+    HIPTRY(c, hipEventRecord(c->ev_user, c->user_stream));
+    HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
+    TRY(ensure_acts(c, rows));
+    TRY(ensure_kv(c, n_images, c->T + 1));
+    TRY(ensure(c, c->meta, kMetaCount * 4));
+    TRY(ensure(c, c->meta_pf, kMetaCount * 4));
+    TRY(ensure(c, c->plen, n_images * 4));
+    TRY(ensure(c, c->labels, n_images * 4));
+    TRY(ensure(c, c->seq_row0, (n_seqs + 1) * 4));
+    TRY(ensure(c, c->seq_img, n_seqs * 4));
+    TRY(ensure(c, c->seq_branch, n_seqs * 4));
+    TRY(ensure(c, c->seg_seq, n_seqs * 4));
+    TRY(ensure(c, c->seg_row0, (n_seqs + 1) * 4));
+    TRY(ensure(c, c->seg_nrows, n_seqs * 4));
+    TRY(ensure(c, c->seg_pos0, n_seqs * 4));
+    TRY(ensure(c, c->seg_pages, (size_t)n_seqs * c->max_pages * 4));
+    std::vector<int32_t> segn(n_seqs), segpos(n_seqs, 0), sbr(n_seqs, 0), mz(kMetaCount, 0);
+    for (int q = 0; q < n_seqs; ++q) segn[q] = row0[q + 1] - row0[q];
+    HIPTRY(c, hipMemcpyAsync(c->meta.p, mz.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->plen.p, check_len.data(), n_images * 4, hipMemcpyHostToDevice, s));
+    check_prefix(tokens, as<int32_t>(c->plen), n_images, c->T, c->V, as<int32_t>(c->meta) + kMetaError, s);
+    int32_t err = 0;
+    HIPTRY(c, hipMemcpyAsync(&err, as<int32_t>(c->meta) + kMetaError, 4, hipMemcpyDeviceToHost, s));
+    HIPTRY(c, hipStreamSynchronize(s));
+    if (err) return fail(HBSJD_EINVAL, "a token is outside [0, vocab)");
+    HIPTRY(c, hipMemcpyAsync(c->labels.p, labels.data(), n_images * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seq_row0.p, row0.data(), (n_seqs + 1) * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seq_img.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seq_branch.p, sbr.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_seq.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, row0.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
+    seg_pages(as<int32_t>(c->seg_seq), n_seqs, as<int32_t>(c->ptab), c->max_pages,
+              as<int32_t>(c->seg_pages), s);
+    std::vector<int32_t> mpf(kMetaCount, 0);
+    mpf[kMetaRows] = rows;
+    mpf[kMetaSegs] = n_seqs;
+    HIPTRY(c, hipMemcpyAsync(c->meta_pf.p, mpf.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
+    HIPTRY(c, hipStreamSynchronize(s));
+    // C is the null class here; the row builder maps branch 0 to labels[image]
+    PrefillRowsArgs pa{n_seqs, c->T, 1, c->C, c->max_pages, rows, as<int32_t>(c->seq_row0),
+                       as<int32_t>(c->seq_img), as<int32_t>(c->seq_branch), tokens,
+                       as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->row_tok),
+                       as<int32_t>(c->row_pos), as<int32_t>(c->row_kv), as<int32_t>(c->row_seq)};
+    prefill_rows(pa, s);
+    int32_t* mp = as<int32_t>(c->meta_pf);
+    FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
+                       as<int32_t>(c->row_seq)},
+               mp + kMetaRows, rows,
+               Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0),
+                        as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
+               mp + kMetaSegs, n_seqs, maxlen};
+    forward_layers(c, fr);
+    HIPTRY(c, hipGetLastError());
     return HBSJD_OK;
 }
 
@@ -1051,82 +1147,121 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
         if (n_seqs < 1 || !tokens || !lens || !labels || !logits)
             return fail(HBSJD_EINVAL, "bad forward arguments");
-        std::vector<int32_t> row0(1, 0), simg, sbr, pl(n_seqs), lab(n_seqs);
-        int maxlen = 0;
+        std::vector<int32_t> simg(n_seqs), ln(n_seqs), lab(n_seqs), row0;
         for (int q = 0; q < n_seqs; ++q) {
             if (lens[q] < 0 || lens[q] > c->T) return fail(HBSJD_EINVAL, "length out of [0, T]");
             if (labels[q] < 0 || labels[q] > c->C) return fail(HBSJD_EINVAL, "label out of [0, n_classes]");
-            simg.push_back(q);
-            sbr.push_back(0);
-            row0.push_back(row0.back() + lens[q] + 1);
-            maxlen = std::max(maxlen, lens[q] + 1);
-            pl[q] = lens[q];
+            simg[q] = q;
+            ln[q] = lens[q];
             lab[q] = labels[q];
         }
-        hipStream_t s = c->stream;
+        TRY(forward_core(c, n_seqs, tokens, lab, ln, simg, ln, row0));
         const int rows = row0.back();
-        c->have_state = false;
-        HIPTRY(c, hipEventRecord(c->ev_user, c->user_stream));
-        HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
-        TRY(ensure_acts(c, rows));
-        TRY(ensure_kv(c, n_seqs, c->T + 1));
-        TRY(ensure(c, c->meta, kMetaCount * 4));
-        TRY(ensure(c, c->meta_pf, kMetaCount * 4));
-        TRY(ensure(c, c->plen, n_seqs * 4));
-        TRY(ensure(c, c->labels, n_seqs * 4));
-        TRY(ensure(c, c->seq_row0, (n_seqs + 1) * 4));
-        TRY(ensure(c, c->seq_img, n_seqs * 4));
-        TRY(ensure(c, c->seq_branch, n_seqs * 4));
-        TRY(ensure(c, c->seg_seq, n_seqs * 4));
-        TRY(ensure(c, c->seg_row0, (n_seqs + 1) * 4));
-        TRY(ensure(c, c->seg_nrows, n_seqs * 4));
-        TRY(ensure(c, c->seg_pos0, n_seqs * 4));
-        TRY(ensure(c, c->seg_pages, (size_t)n_seqs * c->max_pages * 4));
-        std::vector<int32_t> segn(n_seqs), segpos(n_seqs, 0), mz(kMetaCount, 0);
-        for (int q = 0; q < n_seqs; ++q) segn[q] = row0[q + 1] - row0[q];
-        HIPTRY(c, hipMemcpyAsync(c->meta.p, mz.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->plen.p, pl.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        check_prefix(tokens, as<int32_t>(c->plen), n_seqs, c->T, c->V, as<int32_t>(c->meta) + kMetaError, s);
-        int32_t err = 0;
-        HIPTRY(c, hipMemcpyAsync(&err, as<int32_t>(c->meta) + kMetaError, 4, hipMemcpyDeviceToHost, s));
-        HIPTRY(c, hipStreamSynchronize(s));
-        if (err) return fail(HBSJD_EINVAL, "a token is outside [0, vocab)");
-        HIPTRY(c, hipMemcpyAsync(c->labels.p, lab.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seq_row0.p, row0.data(), (n_seqs + 1) * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seq_img.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seq_branch.p, sbr.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seg_seq.p, simg.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seg_row0.p, row0.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seg_nrows.p, segn.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipMemcpyAsync(c->seg_pos0.p, segpos.data(), n_seqs * 4, hipMemcpyHostToDevice, s));
-        seg_pages(as<int32_t>(c->seg_seq), n_seqs, as<int32_t>(c->ptab), c->max_pages,
-                  as<int32_t>(c->seg_pages), s);
-        std::vector<int32_t> mpf(kMetaCount, 0);
-        mpf[kMetaRows] = rows;
-        mpf[kMetaSegs] = n_seqs;
-        HIPTRY(c, hipMemcpyAsync(c->meta_pf.p, mpf.data(), kMetaCount * 4, hipMemcpyHostToDevice, s));
-        HIPTRY(c, hipStreamSynchronize(s));
-        // C is the null class here; the row builder maps branch 0 to labels[b]
-        PrefillRowsArgs pa{n_seqs, c->T, 1, c->C, c->max_pages, rows, as<int32_t>(c->seq_row0),
-                           as<int32_t>(c->seq_img), as<int32_t>(c->seq_branch), tokens,
-                           as<int32_t>(c->labels), as<int32_t>(c->ptab), as<int32_t>(c->row_tok),
-                           as<int32_t>(c->row_pos), as<int32_t>(c->row_kv), as<int32_t>(c->row_seq)};
-        prefill_rows(pa, s);
-        int32_t* mp = as<int32_t>(c->meta_pf);
-        FwdRows fr{RowMeta{as<int32_t>(c->row_tok), as<int32_t>(c->row_pos), as<int32_t>(c->row_kv),
-                           as<int32_t>(c->row_seq)},
-                   mp + kMetaRows, rows,
-                   Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0),
-                            as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
-                   mp + kMetaSegs, n_seqs, maxlen};
-        forward_layers(c, fr);
-        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaRows, rows, logits,
-                    c->b_lm, s);
+        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d,
+                    as<int32_t>(c->meta_pf) + kMetaRows, rows, logits, c->b_lm, c->stream);
         HIPTRY(c, hipGetLastError());
-        HIPTRY(c, hipStreamSynchronize(s));
+        HIPTRY(c, hipStreamSynchronize(c->stream));
         return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_forward");
+    }
+}
+
+hbsjd_status hbsjd_bikl_rows(const float* logits_s, const float* logits_t, int64_t rows,
+                             int32_t V, float* out, void* stream) {
+    try {
+        if (rows < 0 || rows > INT32_MAX || V < 4 || V > kMaxVocab || V % 4 != 0)
+            return fail(HBSJD_EINVAL, "need 0 <= rows < 2^31 and V a multiple of 4 in [4, 16384]");
+        if (rows > 0 && (!logits_s || !logits_t || !out)) return fail(HBSJD_EINVAL, "NULL buffer");
+        hipStream_t s = (hipStream_t)stream;
+        bikl_rows(logits_s, logits_t, (int)rows, V, nullptr, out, s);
+        hipError_t e = hipGetLastError();
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("bikl_rows: ") + hipGetErrorString(e));
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_bikl_rows");
+    }
+}
+
+hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
+                              const int32_t* tokens, const int32_t* prefix_len,
+                              const int32_t* class_labels, float* per_position, float* loss) {
+    try {
+        GUARD(teacher);
+        GUARD(student);
+        if (!student->weights || !teacher->weights) return fail(HBSJD_ESTATE, "weights not loaded");
+        if (student == teacher) return fail(HBSJD_EINVAL, "student and teacher must be two contexts");
+        if (student->device != teacher->device) return fail(HBSJD_EINVAL, "contexts on different GPUs");
+        if (student->T != teacher->T || student->V != teacher->V)
+            return fail(HBSJD_EINVAL, "student and teacher need the same grid and vocabulary");
+        if (B < 1 || !tokens || !prefix_len || !class_labels || !per_position || !loss)
+            return fail(HBSJD_EINVAL, "bad scoring arguments");
+        const int T = student->T, C = std::min(student->C, teacher->C);
+        // sequences: the images with a generated suffix, teacher-forced over
+        // [class, x_1..x_{T-1}]; scored rows: positions k_b..T-1 of each
+        std::vector<int32_t> simg, ln, chk(B, 0), lab(B), kk(B), sel, oidx;
+        for (int b = 0; b < B; ++b) {
+            const int k = prefix_len[b];
+            if (k < 0 || k > T) return fail(HBSJD_EINVAL, "prefix_len out of [0, T]");
+            if (class_labels[b] < 0 || class_labels[b] >= C)
+                return fail(HBSJD_EINVAL, "class label out of [0, n_classes)");
+            lab[b] = class_labels[b];
+            kk[b] = k;
+            if (k == T) continue;
+            simg.push_back(b);
+            ln.push_back(T - 1);
+            chk[b] = T - 1;
+        }
+        hipStream_t s = student->stream;
+        HIPTRY(student, hipEventRecord(student->ev_user, student->user_stream));
+        HIPTRY(student, hipStreamWaitEvent(s, student->ev_user, 0));
+        HIPTRY(student, hipMemsetAsync(per_position, 0, (size_t)B * T * 4, s));
+        const int nq = (int)simg.size();
+        if (nq > 0) {
+            for (int q = 0; q < nq; ++q)
+                for (int p = kk[simg[q]]; p < T; ++p) {
+                    sel.push_back(q * T + p);
+                    oidx.push_back(simg[q] * T + p);
+                }
+            const int nsel = (int)sel.size();
+            hbsjd_ctx* both[2] = {teacher, student};
+            for (hbsjd_ctx* c : both) {
+                std::vector<int32_t> row0;
+                TRY(forward_core(c, B, tokens, lab, chk, simg, ln, row0));
+                TRY(ensure(c, c->lm_idx, (size_t)nsel * 4));
+                TRY(ensure(c, c->score_logits, (size_t)nsel * c->V * 4));
+                HIPTRY(c, hipMemcpyAsync(c->lm_idx.p, sel.data(), (size_t)nsel * 4,
+                                         hipMemcpyHostToDevice, c->stream));
+                int32_t* mp = as<int32_t>(c->meta_pf);
+                HIPTRY(c, hipMemcpyAsync(mp + kMetaActive, &nsel, 4, hipMemcpyHostToDevice, c->stream));
+                rmsnorm(c->bf16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, nsel,
+                        c->g_out, c->m.rms_eps, c->d, c->hb.p, c->stream);
+                gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, nsel,
+                            as<float>(c->score_logits), c->b_lm, c->stream);
+                HIPTRY(c, hipGetLastError());
+            }
+            if (!teacher->ev_done)
+                HIPTRY(teacher, hipEventCreateWithFlags(&teacher->ev_done, hipEventDisableTiming));
+            HIPTRY(teacher, hipEventRecord(teacher->ev_done, teacher->stream));
+            HIPTRY(student, hipStreamWaitEvent(s, teacher->ev_done, 0));
+            TRY(ensure(student, student->score_idx, (size_t)nsel * 4));
+            TRY(ensure(student, student->score_k, (size_t)B * 4));
+            HIPTRY(student, hipMemcpyAsync(student->score_idx.p, oidx.data(), (size_t)nsel * 4,
+                                           hipMemcpyHostToDevice, s));
+            HIPTRY(student, hipMemcpyAsync(student->score_k.p, kk.data(), (size_t)B * 4,
+                                           hipMemcpyHostToDevice, s));
+            bikl_rows(as<float>(student->score_logits), as<float>(teacher->score_logits), nsel,
+                      student->V, as<int32_t>(student->score_idx), per_position, s);
+            bikl_mean(per_position, as<int32_t>(student->score_k), B, T, loss, s);
+        } else {
+            HIPTRY(student, hipMemsetAsync(loss, 0, (size_t)B * 4, s));
+        }
+        HIPTRY(student, hipGetLastError());
+        HIPTRY(student, hipStreamSynchronize(s));   // also keeps the host staging alive
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_score_bikl");
     }
 }
 

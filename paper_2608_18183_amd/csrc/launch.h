@@ -120,6 +120,7 @@ struct RoundSetupArgs {
     int32_t* a_hist;
     int32_t* mode_hist;
     int32_t* seg_pages;
+    int32_t* win_end;   // batch-synchronous windows: [B] end of each image's window; null otherwise
 };
 void round_setup(const RoundSetupArgs& a, hipStream_t s);
 
@@ -177,8 +178,16 @@ struct VerifyArgs {
     int64_t* stats;          // [4]
     int32_t* meta;
     int ar = 0;              // cached-AR rounds: commit one draw of each image's single row
+    const int32_t* win_end = nullptr;   // batch-synchronous windows: verify up to win_end[b]
 };
 void verify_commit(const VerifyArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- teacher scoring
+// per row r: D_biKL(softmax(ls[r]), softmax(lt[r])) into out[out_idx ? out_idx[r] : r]
+void bikl_rows(const float* ls, const float* lt, int rows, int V, const int32_t* out_idx,
+               float* out, hipStream_t s);
+// loss[b] = mean of per[b][t-1] over t = k[b]+1..T (0 when k[b] = T)
+void bikl_mean(const float* per, const int32_t* k, int B, int T, float* loss, hipStream_t s);
 
 void verify_probs(int B, int W, int V, const float* p, const float* q, const int32_t* drafts,
                   const float* u_acc, const float* u_res, int32_t* counts, int32_t* tokens,

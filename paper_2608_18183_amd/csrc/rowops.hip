@@ -20,6 +20,18 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
     __shared__ int s_base;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     if (t == 0) s_base = 0;
+    // batch-synchronous windows: the batch moves on to the next window once no
+    // active image has drafts of its current one left to verify. Every reader
+    // derives the new end from the old one; the owners store it at the end.
+    int pend = 0;
+    if (a.win_end)
+        for (int b = t; b < a.B; b += 1024) pend |= a.cursor[b] < min(a.win_end[b], a.T) ? 1 : 0;
+    const bool advance = a.win_end && !__syncthreads_or(pend);
+    auto window_end = [&](int b) {
+        if (!a.win_end) return a.T;
+        const int e = a.win_end[b];
+        return advance ? min(e + a.W, a.T) : e;
+    };
     __syncthreads();
     for (int c0 = 0; c0 < a.B; c0 += 1024) {
         const int b = c0 + t;
@@ -62,7 +74,7 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
         const int b = a.slot_img[s];
         int n = a.cursor[b];
         n = n > a.T ? a.T : n;
-        const int We = min(a.W, a.T - n);
+        const int We = max(min(a.W, window_end(b) - n), 0);
         const int seq = b * a.cfg + br;
         const int pos = n + i;
         int tok;
@@ -103,6 +115,10 @@ __global__ __launch_bounds__(1024) void k_round_setup(RoundSetupArgs a) {
         } else if (A > 0) {
             atomicOr(&a.meta[kMetaError], (int)kErrRoundOverflow);
         }
+    }
+    if (advance) {
+        __syncthreads();   // every read of the old ends is done
+        for (int b = t; b < a.B; b += 1024) a.win_end[b] = min(a.win_end[b] + a.W, a.T);
     }
 }
 

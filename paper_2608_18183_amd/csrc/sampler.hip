@@ -601,7 +601,9 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
         base = n;
         nrows = 1;
     } else {
-        const int We = min(W, a.T - n);
+        // the batch-synchronous ablation stops at the image's window end; an
+        // image already there verifies nothing and only re-draws its window
+        const int We = max(min(W, (a.win_end ? a.win_end[b] : a.T) - n), 0);
         if (t < W) {
             old_dr[t] = a.drafts[(size_t)b * W + t];
             old_q[t] = a.qsrc[(size_t)b * W + t];
@@ -675,7 +677,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
             if (a.counts && round >= 0 && round < a.max_rounds) a.counts[(size_t)round * a.B + b] = count;
             atomicAdd((unsigned long long*)&a.stats[0], (unsigned long long)count);
             atomicAdd((unsigned long long*)&a.stats[1], (unsigned long long)(rejected ? 1 : 0));
-            atomicAdd((unsigned long long*)&a.stats[2], 1ull);
+            atomicAdd((unsigned long long*)&a.stats[2], count > 0 ? 1ull : 0ull);
             a.cursor[b] = n + count;
         }
         n_new = n + count;

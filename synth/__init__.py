@@ -70,6 +70,12 @@ def _shape_b(grid: int = 16, bias: bool = False) -> ModelShape:
     return ModelShape(12, 768, 12, 2048, 16384, 1000, grid, has_lm_bias=bias)
 
 
+def teacher_shape(student: ModelShape) -> ModelShape:
+    """The teacher of the scoring step: the LlamaGen-L architecture (24 layers,
+    d 1024, 16 heads, f 2816) on the student's grid, vocabulary and classes."""
+    return ModelShape(24, 1024, 16, 2816, student.vocab, student.n_classes, student.grid)
+
+
 WORKLOADS: Dict[str, Workload] = {
     # 2 layers, d 64, 8x8 grid, batch 4, prefix 0-16, W=4, fp32
     "tiny": Workload("tiny", _shape_tiny(), "f32", 4, 4, 24, 0, 0.0,

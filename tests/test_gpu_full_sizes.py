@@ -41,10 +41,11 @@ def _setup(name):
     return wl, shape, blob, batch, ctx
 
 
-def _rollout(ctx, wl, batch, seed, mode, gamma=-1):
+def _rollout(ctx, wl, batch, seed, mode, gamma=-1, progress=0):
     return ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
                              batch.temperature, wl.window, history=wl.history, top_k=wl.top_k,
-                             cfg_scale=wl.cfg_scale, seed=seed, exec_mode=mode, gamma=gamma)
+                             cfg_scale=wl.cfg_scale, seed=seed, exec_mode=mode, gamma=gamma,
+                             progress=progress)
 
 
 def _check_invariants(out, batch, wl, T, V):
@@ -136,3 +137,21 @@ def test_full_size_xl_cfg_rollout_invariants():
     t = _check_invariants(out, batch, wl, shape.T, shape.vocab)
     comp = _rollout(ctx, wl, batch, 1000, P().EXEC_COMPACT)
     assert np.array_equal(comp["tokens"].cpu().numpy(), t)
+
+
+def test_full_size_sync_schedule():
+    """The Batch-Synchronous ablation at the B workload's full size: the
+    shared-window schedule holds and it needs at least as many rounds as the
+    longest suffix needs windows."""
+    from tests.test_oracle_rollout import replay_sync_schedule
+    wl, shape, blob, batch, ctx = _setup("llamagen_b")
+    out = _rollout(ctx, wl, batch, 1000, P().EXEC_AUTO, gamma=wl.batch, progress=P().PROGRESS_SYNC)
+    c = out["counts"].cpu().numpy()
+    n = replay_sync_schedule(c, batch.prefix_len, shape.T, wl.window)
+    assert (n == shape.T).all()
+    tok = out["tokens"].cpu().numpy()
+    for b, k in enumerate(batch.prefix_len):
+        assert np.array_equal(tok[b, :k], batch.prefix_tokens[b, :k])
+    assert (tok >= 0).all() and (tok < shape.vocab).all()
+    L = shape.T - batch.prefix_len
+    assert out["rounds"] >= int(np.ceil(L.max() / wl.window))

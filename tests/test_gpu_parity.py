@@ -291,6 +291,62 @@ def test_rollout_ar_bf16_equals_sjd_window_1():
     assert (a >= 0).all() and (a < shape.vocab).all()
 
 
+# ------------------------------------------------------------------ batch-synchronous windows
+
+
+@pytest.mark.parametrize("W,top_k,greedy,H,mode", [(4, 0, False, 24, "auto"), (3, 5, False, 2, "full"),
+                                                    (4, 0, True, 24, "compact"),
+                                                    (9, 20, False, 3, "auto"), (1, 0, False, 24, "full")])
+def test_rollout_sync_f32_tiny_equals_oracle(tiny, W, top_k, greedy, H, mode):
+    """The Batch-Synchronous SJD ablation (Sec. 4.2, Table 2) against the
+    oracle's shared-window schedule: tokens, per-round counts (0 while an image
+    waits at a boundary), rounds and statistics."""
+    w, blob, om = tiny
+    batch = synth.make_batch(w, 3)
+    batch.prefix_len[1] = 60                 # finishes early
+    m = {"full": P().EXEC_FULL, "compact": P().EXEC_COMPACT, "auto": P().EXEC_AUTO}[mode]
+    ctx = gu.make_ctx(w.model, "f32", blob)
+    g = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                          batch.temperature, W, history=H, top_k=top_k, seed=77,
+                          verify_mode=P().VERIFY_GREEDY if greedy else P().VERIFY_PROB,
+                          exec_mode=m, gamma=2, progress=P().PROGRESS_SYNC)
+    o = om.rollout(batch, W=W, H=H, top_k=top_k, seed=77, greedy=greedy,
+                   exec_mode={P().EXEC_FULL: 0, P().EXEC_COMPACT: 1, P().EXEC_AUTO: 2}[m],
+                   gamma=2, sync=True)
+    assert np.array_equal(g["tokens"].cpu().numpy(), o["tokens"])
+    assert g["rounds"] == o["rounds"]
+    assert np.array_equal(g["counts"].cpu().numpy(), o["counts"])
+    assert np.array_equal(g["active"], o["active"])
+    assert g["verified"] == o["verified"] and g["rejected"] == o["rejected"]
+    assert g["image_rounds"] == o["image_rounds"]
+
+
+def test_rollout_sync_bf16_schedule_and_modes():
+    from tests.test_oracle_rollout import replay_sync_schedule
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 1, batch=8)
+    batch.prefix_len[3] = shape.T - 5
+    ctx = gu.make_ctx(shape, "bf16", blob)
+    outs = [ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                              batch.temperature, wl.window, top_k=wl.top_k, seed=1000,
+                              exec_mode=mode, gamma=4, progress=P().PROGRESS_SYNC)
+            for mode in [P().EXEC_FULL, P().EXEC_COMPACT, P().EXEC_AUTO]]
+    t0 = outs[0]["tokens"].cpu().numpy()
+    c0 = outs[0]["counts"].cpu().numpy()
+    for o in outs[1:]:
+        assert np.array_equal(o["tokens"].cpu().numpy(), t0)
+        assert np.array_equal(o["counts"].cpu().numpy(), c0)
+    n = replay_sync_schedule(c0, batch.prefix_len, shape.T, wl.window)
+    assert (n == shape.T).all()
+    for b in range(8):
+        k = int(batch.prefix_len[b])
+        assert np.array_equal(t0[b, :k], batch.prefix_tokens[b, :k])
+    assert (t0 >= 0).all() and (t0 < shape.vocab).all()
+    assert (c0 == 0).any() and outs[0]["image_rounds"] == int((c0 > 0).sum())
+
+
 # ------------------------------------------------------------------ round API and errors
 
 
