@@ -152,6 +152,8 @@ def main() -> int:
     ap.add_argument("--cpu-images", type=int, default=0, help="images in the CPU sample (0 = auto)")
     ap.add_argument("--ar-steps", type=int, default=2,
                     help="timed rollouts of the cached-AR baseline after the SJD ones (0 = skip)")
+    ap.add_argument("--score-steps", type=int, default=2,
+                    help="timed teacher-scoring calls (Eq. 3) on the completed rollout (0 = skip)")
     ap.add_argument("--ablation-steps", type=int, default=1,
                     help="timed rollouts per execution ablation: Full, Compact, a gamma sweep "
                          "and Batch-Synchronous SJD (0 = skip)")
@@ -284,6 +286,49 @@ def main() -> int:
                 ablations[k]["speedup_vs_cached_ar"] = round(
                     ar["ms_per_step"] / ablations[k]["ms_per_step"], 3)
 
+    # teacher scoring of the completed sequences (Sec. 3.1, Eq. 3): student and
+    # an L-architecture teacher forward, then the per-position biKL kernel,
+    # whose launches are timed with HIP events on the library's stream
+    scoring = None
+    if args.score_steps > 0:
+        tshape = synth.teacher_shape(shape)
+        teacher = P.Context(P.ModelDesc(tshape.n_layers, tshape.d_model, tshape.n_heads,
+                                        tshape.mlp_hidden, tshape.vocab, tshape.n_classes,
+                                        tshape.grid, desc.dtype, False, tshape.rms_eps,
+                                        tshape.rope_base))
+        teacher.hbsjd_load_weights(synth.make_weights(tshape, 5))
+        seqs = out_tokens.clone()
+        ctx.hbsjd_score_bikl(teacher, seqs, batch.prefix_len, batch.labels)
+        torch.cuda.synchronize()
+        ctx.hbsjd_profile_start(["bikl"])
+        t3 = time.perf_counter()
+        for _ in range(args.score_steps):
+            _, loss = ctx.hbsjd_score_bikl(teacher, seqs, batch.prefix_len, batch.labels)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t3) / args.score_steps
+        bms, bn = ctx.hbsjd_profile_read()["bikl"]
+        ctx.hbsjd_profile_start(())
+        avg_s = bms / 1e3 / max(bn, 1)
+        # algorithmic bytes per launch: both fp32 logits rows read once and
+        # one fp32 written per scored position
+        kb = committed_per_step * (2 * shape.vocab * 4 + 4)
+        scoring = {
+            "teacher": f"{tshape.n_layers}L d{tshape.d_model} h{tshape.n_heads} "
+                       f"f{tshape.mlp_hidden} (LlamaGen-L architecture) on the same grid, "
+                       f"random-init",
+            "ms_per_batch": round(1000.0 * dt, 3),
+            "scored_positions": committed_per_step,
+            "value": round(committed_per_step / dt, 1),
+            "unit": "scored positions/s",
+            "mean_loss": round(float(loss.mean()), 6),
+            "bikl_roofline": {"bound": "hbm", "achieved": round(kb / avg_s / 1e9, 2),
+                              "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": round(kb / avg_s / 1e9 / HBM_PEAK_GBS, 5),
+                              "avg_launch_us": round(avg_s * 1e6, 3), "launches": bn,
+                              "bytes_per_launch": kb},
+        }
+        del teacher
+
     value = committed_per_step * args.steps / elapsed
     counts_total = sum(int(r["verified"]) for r in results)    # committed tokens = sum of counts
     image_rounds = sum(r["image_rounds"] for r in results)
@@ -360,6 +405,7 @@ def main() -> int:
         "roofline": roof,
         "cached_ar": ar,
         "ablations": ablations,
+        "teacher_scoring": scoring,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -304,7 +304,8 @@ typedef enum hbsjd_kernel {
     HBSJD_K_LMHEAD = 8,     /* lm_head GEMM (+ bias) */
     HBSJD_K_TRANSFORM = 9,  /* CFG, temperature, top-k, softmax, chunk prefix */
     HBSJD_K_VERIFY = 10,    /* verification, commit, window refresh */
-    HBSJD_K_COUNT = 11
+    HBSJD_K_BIKL = 11,      /* teacher scoring: per-position bidirectional KL (Eq. 3) */
+    HBSJD_K_COUNT = 12
 } hbsjd_kernel;
 
 /*

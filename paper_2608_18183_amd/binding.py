@@ -22,7 +22,7 @@ EXEC_AUTO, EXEC_FULL, EXEC_COMPACT = 0, 1, 2
 VERIFY_PROB, VERIFY_GREEDY, VERIFY_AR, VERIFY_AR_GREEDY = 0, 1, 2, 3
 PROGRESS_INDEPENDENT, PROGRESS_SYNC = 0, 1
 KERNELS = ["setup", "embed", "qkv", "attn", "oproj", "norm", "w13", "w2", "lmhead",
-           "transform", "verify"]
+           "transform", "verify", "bikl"]
 _STATUS = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EHIP", 4: "ESTATE", 5: "EINTERNAL"}
 
 _P = ctypes.c_void_p

@@ -1251,8 +1251,11 @@ hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
                                            hipMemcpyHostToDevice, s));
             HIPTRY(student, hipMemcpyAsync(student->score_k.p, kk.data(), (size_t)B * 4,
                                            hipMemcpyHostToDevice, s));
-            bikl_rows(as<float>(student->score_logits), as<float>(teacher->score_logits), nsel,
-                      student->V, as<int32_t>(student->score_idx), per_position, s);
+            {
+                Timed tm(student, HBSJD_K_BIKL);
+                bikl_rows(as<float>(student->score_logits), as<float>(teacher->score_logits), nsel,
+                          student->V, as<int32_t>(student->score_idx), per_position, s);
+            }
             bikl_mean(per_position, as<int32_t>(student->score_k), B, T, loss, s);
         } else {
             HIPTRY(student, hipMemsetAsync(loss, 0, (size_t)B * 4, s));

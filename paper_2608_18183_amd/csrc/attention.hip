@@ -6,9 +6,14 @@
 //
 // bf16 path (head_dim 64): one workgroup per (segment, query block, head); the
 // four wavefronts split the 64-key tiles (= KV pages) round-robin by absolute
-// tile index, run an online softmax with S = Q K^T and O += P V on
-// v_mfma_f32_16x16x32_bf16, and merge their partials in a fixed order. A row's
-// result therefore depends only on its position and the cache contents.
+// tile index and run an online softmax on v_mfma_f32_16x16x32_bf16 with the
+// scores computed transposed, S^T = K Q^T: lane (g, c16) then owns query
+// column c16 of each 16-query block, so the softmax needs only a two-step
+// exchange across the four lane groups per block, and the probabilities are
+// already laid out as the B operand of O^T = V^T P^T (V is stored transposed in
+// the cache), so they never leave registers. The four partials are merged in a
+// fixed order. A row's result therefore depends only on its position and the
+// cache contents.
 // fp32 path: one wavefront per (row, head), two-pass softmax.
 #include "common.h"
 #include "launch.h"
@@ -29,18 +34,20 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
                                                    Segments seg, const int* __restrict__ nseg_dev,
                                                    int qblocks) {
     constexpr int QR = NMT * 16;   // query rows per block
+    constexpr int LS = QR + 1;     // padded query stride of the parked partials
     const int sb = blockIdx.x, head = blockIdx.y;
     const int sg = sb / qblocks, qblk = sb - sg * qblocks;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    // the segment's metadata, the count and this wavefront's first page are
-    // independent loads (the grid covers the segment capacity, and the page
-    // list is indexed by segment), so they are in flight together
+    // the segment's metadata, the count and the pages of this wavefront's first
+    // two tiles are independent loads (the grid covers the segment capacity, and
+    // the page list is indexed by segment), so they are in flight together
     const int nseg = *nseg_dev;
     const int nrows = seg.nrows[sg];
     const int row0s = seg.row0[sg];
     const int pos0 = seg.pos0[sg];
-    const int page_w = seg.pages[(size_t)sg * maxp + min(w, maxp - 1)];
+    const int page_a = seg.pages[(size_t)sg * maxp + min(w, maxp - 1)];
+    const int page_b = seg.pages[(size_t)sg * maxp + min(w + 4, maxp - 1)];
     if (sg >= nseg) return;
     const int q0 = qblk * QR;
     if (q0 >= nrows) return;
@@ -49,39 +56,44 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
     const int posf = pos0 + q0;
     const int ntiles = (posf + nq - 1) / 64 + 1;
 
-    // LDS: wavefront w owns region w (QR x 64 floats): P (bf16) during the tile
-    // loop, then its partial output for the merge
-    __shared__ __attribute__((aligned(16))) float lds[4 * QR * 64];
+    // wavefront w parks its partial O as [dim][query] in region w
+    __shared__ float lds[4 * 64 * LS];
     __shared__ float mls[4][2][QR];
-    float* Ow = lds + w * QR * 64;
-    uint16_t* Pw = reinterpret_cast<uint16_t*>(Ow);
 
+    // Q as the B operand: lane (g, c16) holds query c16 + 16 i, dims 32 kk + 8 g ..
+    // (rows past the segment load its last row and are zeroed)
     bf16x8_t qf[NMT][2];
 #pragma unroll
     for (int i = 0; i < NMT; ++i) {
         const int r = i * 16 + c16;
+        const int rr = min(r, nq - 1);
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            if (r < nq)
-                qf[i][kk] = load_bf16x8(qb + (size_t)(row0 + r) * d + head * 64 + kk * 32 + 8 * g);
-            else
-                qf[i][kk] = bf16x8_t{};
+            const bf16x8_t x = load_bf16x8(qb + (size_t)(row0 + rr) * d + head * 64 + kk * 32 + 8 * g);
+            qf[i][kk] = r < nq ? x : bf16x8_t{};
         }
     }
+    // O^T accumulators (dims dj*16 + 4 g + v of query c16 + 16 i), the column's
+    // running maximum (equal in its four lanes) and this lane's share of the sum
     f32x4_t o[NMT][4];
-    float mrow[NMT][4], lrow[NMT][4];
+    float m[NMT], l[NMT];
 #pragma unroll
-    for (int i = 0; i < NMT; ++i)
+    for (int i = 0; i < NMT; ++i) {
+        m[i] = -INFINITY;
+        l[i] = 0.f;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            mrow[i][v] = -INFINITY;
-            lrow[i][v] = 0.f;
-            o[i][v] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        }
-
+        for (int dj = 0; dj < 4; ++dj) o[i][dj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    // K rows are fed in a permuted order: A-operand row c16 of 16-key group
+    // j = 2 kk + h is key 32 kk + 8 (c16 >> 2) + 4 h + (c16 & 3). Score element
+    // v of group j in lane (g, c16) is then key 32 kk + 8 g + 4 h + v, and the
+    // eight scores of groups 2 kk, 2 kk + 1 are exactly the keys 32 kk + 8 g ..
+    // + 7 that the B operand of the P V product needs in this lane.
+    const int krow = 8 * (c16 >> 2) + (c16 & 3);
     const size_t page_elems = (size_t)2 * H * 64 * 64;
     for (int tile = w; tile < ntiles; tile += 4) {
-        const int page = tile == w ? page_w : seg.pages[(size_t)sg * maxp + tile];
+        const int page = tile == w ? page_a
+                         : tile == w + 4 ? page_b : seg.pages[(size_t)sg * maxp + tile];
         const uint16_t* Kb = kv + (size_t)page * page_elems + (size_t)head * 4096;
         const uint16_t* Vb = kv + (size_t)page * page_elems + (size_t)(H + head) * 4096;
         // both operands of the tile are fetched before any MFMA so their
@@ -90,9 +102,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                kf[j][kk] = load_bf16x8(Kb + (j * 16 + c16) * 64 + kk * 32 + 8 * g);
-                vf[j][kk] = load_bf16x8(Vb + (j * 16 + c16) * 64 + kk * 32 + 8 * g);
+            for (int kd = 0; kd < 2; ++kd) {
+                kf[j][kd] = load_bf16x8(Kb + (32 * (j >> 1) + 4 * (j & 1) + krow) * 64 + kd * 32 + 8 * g);
+                vf[j][kd] = load_bf16x8(Vb + (j * 16 + c16) * 64 + kd * 32 + 8 * g);
             }
         f32x4_t s[NMT][4];
 #pragma unroll
@@ -100,99 +112,85 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
 #pragma unroll
             for (int i = 0; i < NMT; ++i) s[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk)
+            for (int kd = 0; kd < 2; ++kd)
 #pragma unroll
                 for (int i = 0; i < NMT; ++i)
-                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[i][kk], kf[j][kk], s[i][j],
+                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[j][kd], qf[i][kd], s[i][j],
                                                                       0, 0, 0);
         }
-        // online softmax; lane holds rows 4g+v of key columns c16 + 16 j
+        // online softmax of each query column over the tile's 64 keys
 #pragma unroll
         for (int i = 0; i < NMT; ++i) {
+            const int qr = i * 16 + c16;
+            const int qpos = posf + qr;
+            const bool qok = qr < nq;
+            float mx = -INFINITY;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int r = i * 16 + 4 * g + v;
-                const int qpos = posf + r;
-                float mx = -INFINITY;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int key = tile * 64 + j * 16 + c16;
+                for (int v = 0; v < 4; ++v) {
+                    const int key = tile * 64 + 32 * (j >> 1) + 8 * g + 4 * (j & 1) + v;
                     float x = s[i][j][v] * 0.125f;
-                    if (r >= nq || key > qpos) x = -INFINITY;
+                    if (!qok || key > qpos) x = -INFINITY;
                     s[i][j][v] = x;
                     mx = fmaxf(mx, x);
                 }
-                mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
-                const float mnew = fmaxf(mrow[i][v], mx);
-                const bool none = mnew == -INFINITY;
-                const float alpha = none ? 1.f : __expf(mrow[i][v] - mnew);
-                float ps = 0.f;
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float mnew = fmaxf(m[i], mx);
+            const bool none = mnew == -INFINITY;
+            const float alpha = none ? 1.f : __expf(m[i] - mnew);
+            float ps = 0.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
                     const float pv = none ? 0.f : __expf(s[i][j][v] - mnew);
                     s[i][j][v] = pv;
                     ps += pv;
                 }
-                ps += __shfl_xor(ps, 1, 64);
-                ps += __shfl_xor(ps, 2, 64);
-                ps += __shfl_xor(ps, 4, 64);
-                ps += __shfl_xor(ps, 8, 64);
-                lrow[i][v] = lrow[i][v] * alpha + ps;
-                mrow[i][v] = mnew;
+            l[i] = l[i] * alpha + ps;
+            m[i] = mnew;
 #pragma unroll
-                for (int dj = 0; dj < 4; ++dj) o[i][dj][v] *= alpha;
-            }
+            for (int dj = 0; dj < 4; ++dj) o[i][dj] *= alpha;
         }
-        // P (bf16) to this wave's LDS region as [row][key], read back as A operand
+        // O^T += V^T P^T, the B operand taken from this lane's own probabilities
 #pragma unroll
-        for (int i = 0; i < NMT; ++i)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int i = 0; i < NMT; ++i) {
+                bf16x8_t pf;
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    Pw[(i * 16 + 4 * g + v) * 64 + j * 16 + c16] = f32_to_bf16(s[i][j][v]);
-        // P was written by other lanes of this wavefront: order the LDS writes
-        // before the reads below at wavefront scope
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                for (int e = 0; e < 4; ++e) {
+                    pf[e] = (__bf16)s[i][2 * kk][e];
+                    pf[4 + e] = (__bf16)s[i][2 * kk + 1][e];
+                }
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            bf16x8_t pf[NMT];
-#pragma unroll
-            for (int i = 0; i < NMT; ++i)
-                pf[i] = *reinterpret_cast<const bf16x8_t*>(Pw + (i * 16 + c16) * 64 + kk * 32 + 8 * g);
-#pragma unroll
-            for (int dj = 0; dj < 4; ++dj) {
-#pragma unroll
-                for (int i = 0; i < NMT; ++i)
-                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[i], vf[dj][kk], o[i][dj],
+                for (int dj = 0; dj < 4; ++dj)
+                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dj][kk], pf, o[i][dj],
                                                                        0, 0, 0);
             }
-        }
-        // the next tile (or the partial below) overwrites P: keep those writes
-        // after these reads
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    // the column's sum over its four lanes
+#pragma unroll
+    for (int i = 0; i < NMT; ++i) {
+        l[i] += __shfl_xor(l[i], 16, 64);
+        l[i] += __shfl_xor(l[i], 32, 64);
     }
     // every wavefront parks its partial (o, m, l); a wavefront without tiles
     // parks m = -inf, l = 0
+    float* Ow = lds + w * 64 * LS;
 #pragma unroll
-    for (int i = 0; i < NMT; ++i)
+    for (int i = 0; i < NMT; ++i) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = i * 16 + 4 * g + v;
+        for (int dj = 0; dj < 4; ++dj)
 #pragma unroll
-            for (int dj = 0; dj < 4; ++dj) Ow[r * 64 + dj * 16 + c16] = o[i][dj][v];
-            if (c16 == 0) {
-                mls[w][0][r] = mrow[i][v];
-                mls[w][1][r] = lrow[i][v];
-            }
+            for (int v = 0; v < 4; ++v) Ow[(dj * 16 + 4 * g + v) * LS + i * 16 + c16] = o[i][dj][v];
+        if (g == 0) {
+            mls[w][0][i * 16 + c16] = m[i];
+            mls[w][1][i * 16 + c16] = l[i];
         }
+    }
     __syncthreads();
     // merge the four partials in wave order 0, 1, 2, 3 (tile 0 is wave 0's, so
     // its maximum is finite); wavefront w merges rows w, w + 4, ..., lane = dim
@@ -202,16 +200,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         for (int ww = 1; ww < 4; ++ww) ms = fmaxf(ms, mls[ww][0][r]);
         float sc[4];
         sc[0] = __expf(m0 - ms);
-        float l = sc[0] * mls[0][1][r];
+        float lt = sc[0] * mls[0][1][r];
         for (int ww = 1; ww < 4; ++ww) {
             const float mw = mls[ww][0][r];
             sc[ww] = mw == -INFINITY ? 0.f : __expf(mw - ms);
-            l += sc[ww] * mls[ww][1][r];
+            lt += sc[ww] * mls[ww][1][r];
         }
-        const float inv = 1.0f / l;
-        float a = sc[0] * lds[r * 64 + lane];
-        for (int ww = 1; ww < 4; ++ww) a += sc[ww] * lds[ww * QR * 64 + r * 64 + lane];
-        ob[(size_t)(row0 + r) * d + head * 64 + lane] = f32_to_bf16(a * inv);
+        float a = sc[0] * lds[lane * LS + r];
+        for (int ww = 1; ww < 4; ++ww) a += sc[ww] * lds[ww * 64 * LS + lane * LS + r];
+        ob[(size_t)(row0 + r) * d + head * 64 + lane] = f32_to_bf16(a / lt);
     }
 }
 
