@@ -324,62 +324,81 @@ void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows
     });
 }
 
-template <typename T, int PER>
-__global__ __launch_bounds__(256) void k_reduce_norm(const float* __restrict__ part, int splits,
-                                                     int m_cap, float* __restrict__ h,
-                                                     const int* nrows_dev,
-                                                     const float* __restrict__ g, float eps, int d,
-                                                     T* __restrict__ hb) {
+// One 64-lane block per row. Lane l holds dims 4 l + 256 k .. + 3 for k < NV4,
+// read as float4 (d is a multiple of 4; chunks past d are clamped on load and
+// never stored).
+template <typename T, int NV4>
+__global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ part, int splits,
+                                                    int m_cap, float* __restrict__ h,
+                                                    const int* nrows_dev,
+                                                    const float* __restrict__ g, float eps, int d,
+                                                    T* __restrict__ hb) {
     constexpr int kSplitMax = 4;
-    const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int r = blockIdx.x, lane = threadIdx.x;
     if (r >= m_cap) return;
     // one phase of loads, issued with the row count: every split's partial,
     // the residual and the gain (rows below m_cap are always allocated; rows
     // at or past the count store nothing)
     const int nrows = *nrows_dev;
-    float pz[kSplitMax][PER], hv[PER], gv[PER];
+    const int nv = d >> 2;
+    float4 pz[kSplitMax][NV4], hv[NV4], gv[NV4];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        const int i = lane + 64 * k;
-        const bool in = i < d;
+    for (int k = 0; k < NV4; ++k) {
+        const int c = min(lane + 64 * k, nv - 1);
 #pragma unroll
-        for (int z = 0; z < kSplitMax; ++z)
-            pz[z][k] = (in && z < splits) ? part[((size_t)z * m_cap + r) * d + i] : 0.f;
-        hv[k] = in ? h[(size_t)r * d + i] : 0.f;
-        gv[k] = in ? g[i] : 0.f;
+        for (int z = 0; z < kSplitMax; ++z) {
+            const int zz = min(z, splits - 1);
+            pz[z][k] = reinterpret_cast<const float4*>(part + ((size_t)zz * m_cap + r) * d)[c];
+        }
+        hv[k] = reinterpret_cast<const float4*>(h + (size_t)r * d)[c];
+        gv[k] = reinterpret_cast<const float4*>(g)[c];
     }
     if (r >= nrows) return;
-    float x[PER];
+    float4 x[NV4];
     float ss = 0.f;
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        float acc = pz[0][k];
+    for (int k = 0; k < NV4; ++k) {
+        const bool in = lane + 64 * k < nv;
+        float4 acc = pz[0][k];
 #pragma unroll
         for (int z = 1; z < kSplitMax; ++z)
-            if (z < splits) acc += pz[z][k];    // split order
-        x[k] = hv[k] + acc;
-        ss = fmaf(x[k], x[k], ss);
+            if (z < splits) {   // split order
+                acc.x += pz[z][k].x;
+                acc.y += pz[z][k].y;
+                acc.z += pz[z][k].z;
+                acc.w += pz[z][k].w;
+            }
+        x[k] = make_float4(hv[k].x + acc.x, hv[k].y + acc.y, hv[k].z + acc.z, hv[k].w + acc.w);
+        if (in) {
+            ss = fmaf(x[k].x, x[k].x, ss);
+            ss = fmaf(x[k].y, x[k].y, ss);
+            ss = fmaf(x[k].z, x[k].z, ss);
+            ss = fmaf(x[k].w, x[k].w, ss);
+        }
     }
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        const int i = lane + 64 * k;
-        if (i < d) h[(size_t)r * d + i] = x[k];
-    }
+    for (int k = 0; k < NV4; ++k)
+        if (lane + 64 * k < nv) reinterpret_cast<float4*>(h + (size_t)r * d)[lane + 64 * k] = x[k];
     if (!hb) return;
     ss = wave_sum(ss);
     const float rn = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-        const int i = lane + 64 * k;
-        if (i < d) Elem<T>::store(hb + (size_t)r * d + i, (x[k] * rn) * gv[k]);
+    for (int k = 0; k < NV4; ++k) {
+        const int i = 4 * (lane + 64 * k);
+        if (i < d) {
+            Elem<T>::store(hb + (size_t)r * d + i + 0, (x[k].x * rn) * gv[k].x);
+            Elem<T>::store(hb + (size_t)r * d + i + 1, (x[k].y * rn) * gv[k].y);
+            Elem<T>::store(hb + (size_t)r * d + i + 2, (x[k].z * rn) * gv[k].z);
+            Elem<T>::store(hb + (size_t)r * d + i + 3, (x[k].w * rn) * gv[k].w);
+        }
     }
 }
 
-template <typename T, int PER>
+template <typename T, int NV4>
 static void reduce_norm_launch(const float* part, int splits, int m_cap, float* h,
                                const int* nrows_dev, const float* gain, float eps, int d, void* hb,
                                hipStream_t s) {
-    launch(k_reduce_norm<T, PER>, dim3((m_cap + 3) / 4), dim3(256), 0, s, part, splits, m_cap, h,
+    launch(k_reduce_norm<T, NV4>, dim3(m_cap), dim3(64), 0, s, part, splits, m_cap, h,
            nrows_dev, gain, eps, d, (T*)hb);
 }
 
@@ -387,19 +406,14 @@ template <typename T>
 static void reduce_norm_dispatch(const float* part, int splits, int m_cap, float* h,
                                  const int* nrows_dev, const float* gain, float eps, int d,
                                  void* hb, hipStream_t s) {
-    const int per = (d + 63) / 64;
-    if (per <= 1)
-        reduce_norm_launch<T, 1>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
-    else if (per <= 4)
-        reduce_norm_launch<T, 4>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
-    else if (per <= 12)
-        reduce_norm_launch<T, 12>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
-    else if (per <= 16)
-        reduce_norm_launch<T, 16>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
-    else if (per <= 20)
-        reduce_norm_launch<T, 20>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
-    else
-        reduce_norm_launch<T, 24>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
+    switch ((d + 255) / 256) {
+        case 1: reduce_norm_launch<T, 1>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+        case 2: reduce_norm_launch<T, 2>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+        case 3: reduce_norm_launch<T, 3>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+        case 4: reduce_norm_launch<T, 4>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+        case 5: reduce_norm_launch<T, 5>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+        default: reduce_norm_launch<T, 6>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s); break;
+    }
 }
 
 void reduce_residual_norm(bool bf16, const float* part, int splits, int m_cap, float* h,
