@@ -357,6 +357,9 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
 // activation buffers for `rows` rows
 hbsjd_status ensure_acts(hbsjd_ctx* c, long rows) {
     const size_t d = c->d, f = c->f;
+    // kernels index activation rows with 32-bit element offsets
+    if ((size_t)rows * std::max(3 * d, 2 * f) > (size_t)INT32_MAX)
+        return fail(HBSJD_EINVAL, "too many rows in one forward for 32-bit element offsets");
     TRY(ensure(c, c->h, rows * d * 4));
     TRY(ensure(c, c->hb, rows * d * c->esz));
     TRY(ensure(c, c->qb, rows * d * c->esz));
@@ -379,6 +382,9 @@ hbsjd_status ensure_kv(hbsjd_ctx* c, int n_seq, int cap) {
     const long pages = (long)n_seq * c->max_pages;
     const long page_elems = 2L * kPage * c->d;
     c->kv_layer_elems = pages * page_elems;
+    // kernels address a layer's pool with 32-bit element offsets
+    if (c->kv_layer_elems > (long)INT32_MAX)
+        return fail(HBSJD_EINVAL, "KV pool of one layer above 2^31 elements");
     const size_t bytes = (size_t)c->L * c->kv_layer_elems * c->esz;
     if (c->max_kv_bytes && bytes > c->max_kv_bytes)
         return fail(HBSJD_ENOMEM, "KV cache needs " + std::to_string(bytes) +

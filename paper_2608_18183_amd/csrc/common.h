@@ -60,9 +60,12 @@ template <> struct Elem<float> {
     __device__ static float load(const float* p) { return *p; }
     __device__ static void store(float* p, float v) { *p = v; }
 };
+// the device conversion uses the hardware's round-to-nearest-even convert;
+// it agrees with f32_to_bf16 on every finite value
+__device__ inline uint16_t f32_to_bf16_rne(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 template <> struct Elem<uint16_t> {
     __device__ static float load(const uint16_t* p) { return bf16_to_f32(*p); }
-    __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+    __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
 };
 
 // ------------------------------------------------------------ Philox4x32-10

@@ -37,46 +37,51 @@ struct EpiQkv {
     const float* rs;
     int d, heads, dh, T_;
     int part = 0;   // 0 q, 1 k, 2 v: fixed per tile since d is a multiple of the tile width
-    struct Row { int p, slot; };
+    // the bf16 path has head_dim 64; the fp32 path takes it at run time
+    static constexpr int kDh = sizeof(T) == 2 ? 64 : 0;
+    __device__ int head_dim() const { return kDh ? kDh : dh; }
+    // element offsets are 32-bit (the host keeps every activation buffer and a
+    // layer's KV pool below 2^31 elements). A row carries its position and the
+    // offset of its entry for this tile's part (q row; K slot of head 0; V^T
+    // column of head 0), so an element only adds its column part.
+    struct Row { int p, off; };
     struct Aux { float cs, sn; };
     __device__ void begin_tile(int n0) { part = n0 / d; }
     __device__ Row row_info(int m) const {
-        int p = pos[m];
-        return Row{p > T_ ? T_ : p, kvslot[m]};
+        const int p = pos[m], slot = kvslot[m];
+        const int dhv = head_dim();
+        const int page = slot >> 6, s = slot & 63;
+        const int base = page * (2 * heads * 64 * dhv);
+        const int off = part == 0 ? m * d : part == 1 ? base + s * dhv : base + heads * 64 * dhv + s;
+        return Row{p > T_ ? T_ : p, off};
     }
     // loads unconditionally (the V part reads an entry it ignores) so the GEMM's
     // load pipeline sees the same number of loads on every path
     __device__ Aux aux(const Row& ri, int n) const {
+        const int dhv = head_dim();
         const int c = n - part * d;
-        const int e = dh == 64 ? c & 63 : c % dh;
-        const int pi = part < 2 ? ri.p * (dh >> 1) + (e >> 1) : 0;
+        const int e = kDh ? c & (kDh - 1) : c % dhv;
+        const int pi = part < 2 ? ri.p * (dhv >> 1) + (e >> 1) : 0;
         return Aux{rc[pi], rs[pi]};
     }
     __device__ void store(const Row& ri, const Aux& ax, int m, int n, float v, float partner) const {
+        const int dhv = head_dim();
         const int c = n - part * d;
-        const int head = dh == 64 ? c >> 6 : c / dh;
-        const int e = c - head * dh;
+        const int head = kDh ? c / kDh : c / dhv;
+        const int e = c - head * dhv;
         float out = v;
         if (part < 2) {
             const float cs = ax.cs, sn = ax.sn;
             // adjacent pair (2i, 2i+1) turned by the row/column angle of position p
             out = (e & 1) ? (partner * sn + v * cs) : (v * cs - partner * sn);
         }
-        if (part == 0) {
-            Elem<T>::store(q + (size_t)m * d + c, out);
-            return;
-        }
-        const int page = ri.slot >> 6, s = ri.slot & 63;
-        const size_t base = (size_t)page * (2 * heads * 64 * dh);
-        if (part == 1)
-            Elem<T>::store(kv + base + (size_t)head * 64 * dh + (size_t)s * dh + e, out);
-        else
-            Elem<T>::store(kv + base + (size_t)(heads + head) * 64 * dh + (size_t)e * 64 + s, out);
+        const int col = part == 0 ? c : part == 1 ? head * 64 * dhv + e : head * 64 * dhv + e * 64;
+        Elem<T>::store((part == 0 ? q : kv) + (ri.off + col), out);
     }
     __device__ void operator()(int m, int n, float v, float partner) const {
         EpiQkv e = *this;
         e.part = n / d;
-        const Row ri = row_info(m);
+        const Row ri = e.row_info(m);
         e.store(ri, e.aux(ri, n), m, n, v, partner);
     }
 };
@@ -325,7 +330,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const float val = acc[i][j][v];
-                const float partner = __shfl_xor(val, 1, 64);
+                // the neighbouring column's value (lane ^ 1) through a DPP quad
+                // permute [1, 0, 3, 2] rather than an LDS permute
+                const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
+                    0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
                 if (ok) epi.store(rinfo[i][v], aux[i][v][j], row, col0 + j * 16, val, partner);
             }
         }
