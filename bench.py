@@ -111,12 +111,16 @@ def measured_traffic(cls):
     """HBM bytes per launch of a kernel class from the committed counter
     summary (profiles/hbm_traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled
     by a copy of known size), or None when there is none or the kernel's
-    source changed since the counters were taken."""
+    source (its file and the two shared headers) changed since the counters
+    were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    csrc = os.path.join(ROOT, "paper_2608_18183_amd", "csrc")
     try:
         rec = json.load(open(path))[cls]
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        src = b"".join(open(f, "rb").read() for f in
+                       [os.path.join(ROOT, rec["source"]), os.path.join(csrc, "common.h"),
+                        os.path.join(csrc, "launch.h")])
     except (OSError, KeyError, ValueError):
         return None
     if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:

@@ -130,6 +130,10 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     const int s = r / a.rows_per_slot, i = r - s * a.rows_per_slot;
     const int b = a.slot_img[s];
     const float tau = a.temperature[b];
+    // the draw below needs the image's cursor and the seed: fetched now, with
+    // the row, rather than after the reductions
+    const int pos = min(a.cursor[b], a.T) + i + 1;
+    const float u_draft = uniforms_at(meta_seed(a.meta), b, pos).draft;
     const float* lc = a.logits + (size_t)((s * a.cfg) * a.rows_per_slot + i) * V;
     const float* lu = a.cfg == 2 ? a.logits + (size_t)((s * 2 + 1) * a.rows_per_slot + i) * V : nullptr;
 
@@ -356,10 +360,9 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     // matter how the round's verification ends, so its draw from p with
     // u_draft(b, n_b + i + 1) is taken here, with the row's own prefix; the
     // same search as wave_sample_cp, hence the same token
-    const int pos = min(a.cursor[b], a.T) + i + 1;
     int z_draft = -1;
     if (pos <= a.T) {
-        const float target = uniforms_at(meta_seed(a.meta), b, pos).draft * tot[nC];
+        const float target = u_draft * tot[nC];
         if (t < 64) {
             int cs = 0x7fffffff;
             for (int c = t; c < nC; c += 64)
@@ -380,19 +383,28 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
                     *reinterpret_cast<float4*>(&cand[k]) = make_float4(y[k], y[k + 1], y[k + 2], y[k + 3]);
             }
             __syncthreads();
-            if (t < 64) {
-                const float pv = cand[t];
+            if (t == 0) {   // the chunk's entries in order; LDS loads issued ahead of the adds
                 const float before = tot[cs];
+                const int nk = min(kChunk, V - cs * kChunk);
+                float xb[kChunk];
+#pragma unroll
+                for (int k = 0; k < kChunk; k += 4) {
+                    const float4 q4 = *reinterpret_cast<const float4*>(&cand[k]);
+                    xb[k] = q4.x;
+                    xb[k + 1] = q4.y;
+                    xb[k + 2] = q4.z;
+                    xb[k + 3] = q4.w;
+                }
                 float inner = 0.f;
                 int found = -1, lastpos = -1;
-                for (int k = 0; k < kChunk; ++k) {
-                    const float x = __shfl(pv, k, 64);
-                    if (cs * kChunk + k >= V) break;
-                    inner = inner + x;
-                    if (x > 0.f) lastpos = cs * kChunk + k;
-                    if (before + inner > target) { found = cs * kChunk + k; break; }
-                }
-                if (t == 0) s_int[1] = found >= 0 ? found : lastpos;
+#pragma unroll
+                for (int k = 0; k < kChunk; ++k)
+                    if (found < 0 && k < nk) {
+                        inner = inner + xb[k];
+                        if (xb[k] > 0.f) lastpos = cs * kChunk + k;
+                        if (before + inner > target) found = cs * kChunk + k;
+                    }
+                s_int[1] = found >= 0 ? found : lastpos;
             }
             __syncthreads();
             z_draft = s_int[1];
