@@ -72,8 +72,8 @@ typedef enum hbsjd_verify_mode {
 } hbsjd_verify_mode;
 
 /*
- * How images move through their windows (Sec. 4.2, "From Single-Sequence to
- * Batched SJD"; Fig. 1; Table 2).
+ * How images move through their windows (Sec. 4.1, "From Single-Sequence to
+ * Batched SJD"; Fig. 2; Table 2).
  */
 typedef enum hbsjd_progress {
     /* HB-SJD: every image keeps its own cursor and window and advances by its

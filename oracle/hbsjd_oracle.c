@@ -30,8 +30,8 @@
  *    fused guided logits (same paragraph);
  *  - Full vs Compact execution differ only in which rows are physically
  *    processed; the per-round choice is Full iff A > gamma  (Sec. 4.3, Eq. 6);
- *  - the Batch-Synchronous SJD ablation (Sec. 4.2 "From Single-Sequence to
- *    Batched SJD", Fig. 1a, Table 2): every image works through the same
+ *  - the Batch-Synchronous SJD ablation (Sec. 4.1 "From Single-Sequence to
+ *    Batched SJD", Fig. 2a, Table 2): every image works through the same
  *    sequence of Jacobi windows; an image that has committed its whole current
  *    window waits until every active image has done so, and only then does the
  *    batch move on to the next window.

@@ -298,7 +298,7 @@ def test_rollout_ar_bf16_equals_sjd_window_1():
                                                     (4, 0, True, 24, "compact"),
                                                     (9, 20, False, 3, "auto"), (1, 0, False, 24, "full")])
 def test_rollout_sync_f32_tiny_equals_oracle(tiny, W, top_k, greedy, H, mode):
-    """The Batch-Synchronous SJD ablation (Sec. 4.2, Table 2) against the
+    """The Batch-Synchronous SJD ablation (Sec. 4.1, Table 2) against the
     oracle's shared-window schedule: tokens, per-round counts (0 while an image
     waits at a boundary), rounds and statistics."""
     w, blob, om = tiny

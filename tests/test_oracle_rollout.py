@@ -105,8 +105,8 @@ def test_images_are_independent(tiny):
 
 
 def replay_sync_schedule(counts, prefix_len, T, W):
-    """Replays per-round counts against the shared-window rule (Sec. 4.2,
-    Fig. 1a): image b's window w ends at min(k_b + (w+1) W, T); the batch moves
+    """Replays per-round counts against the shared-window rule (Sec. 4.1,
+    Fig. 2a): image b's window w ends at min(k_b + (w+1) W, T); the batch moves
     to window w+1 only when every active image has reached the end of window w;
     until then an image at its boundary commits nothing. Returns the final
     cursors."""
