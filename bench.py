@@ -218,9 +218,12 @@ def main() -> int:
     # timed region: only the dominant class is bracketed by events
     ctx.hbsjd_profile_start([dominant])
     results = []
+    step_s = []   # each rollout call is blocking, so the host clock brackets it
     t0 = time.perf_counter()
     for i in range(args.steps):
+        ts = time.perf_counter()
         results.append(step(1000 + i))
+        step_s.append(time.perf_counter() - ts)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     dom_ms, dom_n = ctx.hbsjd_profile_read()[dominant]
@@ -404,6 +407,12 @@ def main() -> int:
                    "parallelism": "single GPU"},
         "mean_accepted_tokens_per_round": round(mean_accepted, 4),
         "rounds_per_step": rounds,
+        "step_ms": {"per_seed": [round(1000.0 * x, 3) for x in step_s],
+                    "mean": round(1000.0 * float(np.mean(step_s)), 3),
+                    "median": round(1000.0 * float(np.median(step_s)), 3),
+                    "p95": round(1000.0 * float(np.percentile(step_s, 95)), 3)},
+        "active_per_round": [int(x) for x in results[0]["active"]],
+        "mode_per_round": "".join("F" if int(x) == 0 else "C" for x in results[0]["mode"]),
         "reject_rate": round(reject_rate, 4),
         "committed_tokens_per_step": committed_per_step,
         "roofline": roof,

@@ -350,14 +350,16 @@ def test_rollout_sync_bf16_schedule_and_modes():
 # ------------------------------------------------------------------ round API and errors
 
 
-def test_round_api_matches_rollout(tiny):
+@pytest.mark.parametrize("sync", [False, True])
+def test_round_api_matches_rollout(tiny, sync):
     w, blob, om = tiny
     batch = synth.make_batch(w, 1)
     ctx = gu.make_ctx(w.model, "f32", blob)
+    prog = P().PROGRESS_SYNC if sync else P().PROGRESS_INDEPENDENT
     full = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
-                             batch.temperature, 4, seed=1000)
+                             batch.temperature, 4, seed=1000, progress=prog)
     ctx.hbsjd_rollout_begin(gu.device_batch(batch), batch.prefix_len, batch.labels,
-                            batch.temperature, 4, seed=1000)
+                            batch.temperature, 4, seed=1000, progress=prog)
     st = ctx.hbsjd_get_state()
     assert np.array_equal(st["cursors"], batch.prefix_len)
     assert np.all(st["reused"][:, 0] == 1)
@@ -375,6 +377,33 @@ def test_round_api_matches_rollout(tiny):
             break
     assert r == full["rounds"]
     assert np.array_equal(st["tokens"], full["tokens"].cpu().numpy())
+
+
+def test_graph_replays_equal_eager_launches(monkeypatch):
+    """Rounds run as two captured HIP graphs replayed every round (and across
+    rollouts); a context created with HBSJD_NO_GRAPHS=1 launches the same
+    kernels eagerly. Several rollouts, alternated between the two contexts so
+    eager work and synchronisations sit between the replays, must agree bit for
+    bit in tokens and per-round counts."""
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 3, batch=8)
+    batch.prefix_len[2] = shape.T - 3
+    graph = gu.make_ctx(shape, "bf16", blob)
+    monkeypatch.setenv("HBSJD_NO_GRAPHS", "1")
+    eager = gu.make_ctx(shape, "bf16", blob)
+    monkeypatch.delenv("HBSJD_NO_GRAPHS")
+    for seed, mode, prog in [(1000, P().EXEC_AUTO, P().PROGRESS_INDEPENDENT),
+                             (1001, P().EXEC_FULL, P().PROGRESS_INDEPENDENT),
+                             (1002, P().EXEC_AUTO, P().PROGRESS_SYNC),
+                             (1000, P().EXEC_COMPACT, P().PROGRESS_INDEPENDENT)]:
+        outs = [c.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                                batch.temperature, wl.window, top_k=wl.top_k, seed=seed,
+                                exec_mode=mode, gamma=4, progress=prog) for c in (graph, eager)]
+        assert np.array_equal(outs[0]["tokens"].cpu().numpy(), outs[1]["tokens"].cpu().numpy())
+        assert np.array_equal(outs[0]["counts"].cpu().numpy(), outs[1]["counts"].cpu().numpy())
+        assert outs[0]["rounds"] == outs[1]["rounds"] and outs[0]["rounds"] > 2
 
 
 def test_argument_errors(tiny):
