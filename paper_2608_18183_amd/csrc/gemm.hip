@@ -39,6 +39,9 @@ struct EpiQkv {
     int part = 0;   // 0 q, 1 k, 2 v: fixed per tile since d is a multiple of the tile width
     // the bf16 path has head_dim 64; the fp32 path takes it at run time
     static constexpr int kDh = sizeof(T) == 2 ? 64 : 0;
+    // the RoPE factors are fetched after the main loop: holding them through it
+    // costs more (register pressure) than the one exposed load
+    static constexpr bool kLateAux = true;
     __device__ int head_dim() const { return kDh ? kDh : dh; }
     // element offsets are 32-bit (the host keeps every activation buffer and a
     // layer's KV pool below 2^31 elements). A row carries its position and the
@@ -159,6 +162,14 @@ struct EpiLogits {
 // With splits > 1 the K range is cut into equal contiguous parts and each part
 // writes fp32 partial sums to `part` ([split][M][N]) instead of calling the
 // epilogue; the caller's reduce kernel adds the parts in split order.
+// An epilogue may opt out of fetching its per-element inputs before the main
+// loop (static constexpr bool kLateAux = true): they are then fetched after it,
+// which frees their registers during the loop at the cost of one exposed load.
+template <typename E>
+constexpr auto epi_prefetches_aux(int) -> decltype(E::kLateAux, bool()) { return !E::kLateAux; }
+template <typename E>
+constexpr bool epi_prefetches_aux(long) { return true; }
+
 template <int BM, int BN, int WGM, int WGN, int NS, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
                                                    const uint16_t* __restrict__ W, int N, int K,
@@ -252,7 +263,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     // epilogue inputs: row metadata first, then the first tiles, then the
     // per-element tables that depend on the row metadata
     const int col0 = n0 + wn * WN + (lane & 15);
-    constexpr bool kPrefetchAux = TM * TN <= 4;
+    constexpr bool kPrefetchAux = TM * TN <= 4 && epi_prefetches_aux<Epi>(0);
     epi.begin_tile(n0);
     typename Epi::Row rinfo[TM][4];
     typename Epi::Aux aux[TM][4][TN];
