@@ -163,9 +163,9 @@ def main() -> int:
                          "and Batch-Synchronous SJD (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the rollout shards by image with no "
-              f"cross-GPU exchange, and this build measures the single-GPU path "
-              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the rollout "
+              f"shards by image with no cross-GPU exchange, so each GPU would run its own "
+              f"images as an independent single-GPU rollout", file=sys.stderr)
         return 2
 
     import torch
