@@ -321,6 +321,23 @@ def test_rollout_sync_f32_tiny_equals_oracle(tiny, W, top_k, greedy, H, mode):
     assert g["image_rounds"] == o["image_rounds"]
 
 
+def test_rollout_sync_f32_cfg_equals_oracle():
+    shape = synth.small_shape(n_layers=2, d_model=32, n_heads=2, mlp_hidden=48, vocab=64,
+                              n_classes=4, grid=4)
+    blob = synth.make_weights(shape, 3, std=0.2)
+    om = oracle.Model(shape, blob)
+    w = synth.Workload("t", shape, "f32", 6, 3, 2, 7, 2.0, prefix_lo=0, prefix_hi=9)
+    batch = synth.make_batch(w, 5)
+    ctx = gu.make_ctx(shape, "f32", blob)
+    g = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                          batch.temperature, 3, history=2, top_k=7, cfg_scale=2.0, seed=78,
+                          exec_mode=P().EXEC_AUTO, gamma=2, progress=P().PROGRESS_SYNC)
+    o = om.rollout(batch, W=3, H=2, top_k=7, cfg_scale=2.0, seed=78, exec_mode=2, gamma=2,
+                   sync=True)
+    assert np.array_equal(g["tokens"].cpu().numpy(), o["tokens"])
+    assert np.array_equal(g["counts"].cpu().numpy(), o["counts"])
+
+
 def test_rollout_sync_bf16_schedule_and_modes():
     from tests.test_oracle_rollout import replay_sync_schedule
     wl = synth.WORKLOADS["llamagen_b"]

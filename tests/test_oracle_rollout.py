@@ -138,6 +138,18 @@ def test_sync_greedy_equals_greedy_ar(tiny, W, H):
                           np.full(len(b.prefix_len), w.model.T))
 
 
+def test_sync_greedy_with_cfg_equals_greedy_ar():
+    shape = synth.small_shape(n_layers=2, d_model=32, n_heads=2, mlp_hidden=48, vocab=40,
+                              n_classes=4, grid=4)
+    om = oracle.Model(shape, synth.make_weights(shape, 3, std=0.2))
+    w = synth.Workload("t", shape, "f32", 6, 3, 2, 7, 2.0, prefix_lo=0, prefix_hi=9)
+    b = _batch(w, 5)
+    r = om.rollout(b, W=3, H=2, top_k=7, cfg_scale=2.0, seed=77, greedy=True, sync=True)
+    ar = om.rollout_ar(b, top_k=7, cfg_scale=2.0, seed=77, greedy=True)
+    assert np.array_equal(r["tokens"], ar)
+    replay_sync_schedule(r["counts"], b.prefix_len, shape.T, 3)
+
+
 @pytest.mark.parametrize("seed", [1000, 1001])
 def test_sync_window_one_is_token_by_token_sampling(tiny, seed):
     w, _, om = tiny
