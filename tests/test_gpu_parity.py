@@ -439,7 +439,8 @@ def test_argument_errors(tiny):
     bad = [dict(window=0), dict(history=0), dict(top_k=-1), dict(max_rounds=3),
            dict(prefix_len=np.array([0, 0, 0, 65])), dict(class_labels=np.array([0, 0, 0, 10])),
            dict(temperature=np.array([1, 1, 0, 1.0])),
-           dict(temperature=np.array([1, 1, np.nan, 1.0]))]
+           dict(temperature=np.array([1, 1, np.nan, 1.0])), dict(progress=2),
+           dict(progress=-1), dict(exec_mode=3), dict(verify_mode=4)]
     for kw in bad:
         with pytest.raises(E) as ei:
             call(**kw)
