@@ -3,8 +3,9 @@
 // fused into the epilogue (2D RoPE and the paged KV append after QKV, the
 // residual add after O and W2, SwiGLU after W1|W3, bias after the lm_head).
 //
-// bf16 path: 256-thread workgroups, 2x2 wavefronts, LDS-staged double-buffered
-// 64-deep K tiles with an XOR swizzle, v_mfma_f32_16x16x32_bf16 with fp32
+// bf16 path: 256-thread workgroups, 2x2 wavefronts, LDS-staged 64-deep K
+// tiles with an XOR swizzle (loaded straight into LDS for the 64x64 tile,
+// through registers for the 128x128 one), v_mfma_f32_16x16x32_bf16 with fp32
 // accumulation. Every output element sums its K range in the same order no
 // matter how many rows the launch has or where the row sits, so a row's result
 // does not depend on the rest of the batch.
@@ -148,17 +149,30 @@ struct EpiLogits {
 };
 
 // ---------------------------------------------------------------- bf16 MFMA
-// Workgroup tile BM x BN, 4 wavefronts arranged WGM x WGN, 64-deep K steps.
-// Tiles are staged global -> registers -> LDS (XOR-swizzled 16-byte chunks,
-// double-buffered); NS register stages keep NS-2 tiles in flight behind the
-// one being written to LDS, so a step does not wait a full memory round trip.
-// That only holds if every step issues the same loads on every path: the
-// compiler's wait counts are per wavefront and in issue order, and a load
-// skipped on some path forces it to wait for everything. So the steady loop
-// has no conditional loads: rows past M re-read row M-1 (their products land
-// in rows that are never stored) and steps past the end re-read the last K
-// tile. The epilogue's own inputs (row metadata, RoPE tables, bias) are
-// fetched before the main loop so their latency hides behind it.
+// Workgroup tile BM x BN, 4 wavefronts arranged WGM x WGN, 64-deep K steps,
+// operands in LDS as rows of eight 16-byte chunks, chunk c of row r stored at
+// position c ^ (r & 7) so the MFMA operand reads fall in distinct banks.
+// Two ways of filling LDS, chosen per tile size:
+//  * direct (kDirect): each 16-byte chunk goes from global memory straight to
+//    LDS (global_load_lds_dwordx4), NS LDS stages deep, so NS-2 tiles are in
+//    flight behind the one being multiplied and no registers hold them. The
+//    hardware writes lane l's chunk at 16 l bytes past the wavefront's LDS
+//    address, so each lane fetches the global chunk whose swizzled position
+//    is l. The waits are explicit: before step kt a wavefront waits until at
+//    most (NS-2) tiles' loads of its own are outstanding (loads complete in
+//    issue order), then a bare s_barrier makes every wavefront's part of tile
+//    kt visible. (__syncthreads would add a release fence, which waits for
+//    every outstanding LDS-bound load.) A stage is refilled only after the
+//    barrier that follows the step that read it.
+//  * register staging: global -> registers -> LDS, double-buffered, with NS
+//    register stages keeping NS-2 tiles in flight.
+// Either way every step issues the same loads on every path: wait counts are
+// per wavefront and in issue order, and a load skipped on some path forces a
+// wait for everything. So the steady loop has no conditional loads: rows past
+// M re-read row M-1 (their products land in rows that are never stored) and
+// the register path's steps past the end re-read the last K tile. The
+// epilogue's own inputs (row metadata, RoPE tables, bias) are fetched before
+// the main loop so their latency hides behind it.
 // With splits > 1 the K range is cut into equal contiguous parts and each part
 // writes fp32 partial sums to `part` ([split][M][N]) instead of calling the
 // epilogue; the caller's reduce kernel adds the parts in split order.
@@ -170,7 +184,23 @@ constexpr auto epi_prefetches_aux(int) -> decltype(E::kLateAux, bool()) { return
 template <typename E>
 constexpr bool epi_prefetches_aux(long) { return true; }
 
-template <int BM, int BN, int WGM, int WGN, int NS, typename Epi>
+// one 16-byte chunk per lane from global memory to LDS: lane l's chunk lands
+// at lds + 16 l (lds is the same for the whole wavefront)
+__device__ __forceinline__ void load_to_lds16(const void* g, void* lds) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+// workgroup barrier alone; the memory clobber keeps the compiler from moving
+// LDS accesses across it
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// wait until at most N vector memory loads of this wavefront are outstanding
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    // s_waitcnt fields: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at [15:14]
+    __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
+template <int BM, int BN, int WGM, int WGN, int NS, bool kDirect, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
                                                    const uint16_t* __restrict__ W, int N, int K,
                                                    const int* __restrict__ m_dev, int m_cap,
@@ -179,8 +209,9 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 16, TN = WN / 16;
     constexpr int LA = BM / 32, LB = BN / 32;   // 16-byte chunks per thread per tile
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * BK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * BK];
+    constexpr int STAGE = (BM + BN) * BK;       // elements of one A + B stage
+    // direct: NS stages; register staging: 2
+    __shared__ __attribute__((aligned(1024))) uint16_t S[(kDirect ? NS : 2) * STAGE];
 
     const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
     const int tiles_m = (m_cap + BM - 1) / BM;
@@ -202,33 +233,6 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int wm = wv / WGN, wn = wv % WGN;
-    const int lc = t & 7, lr = t >> 3;
-
-    u32x4_t R[NS][LA + LB];
-    auto gload = [&](u32x4_t* r, int kt) {
-        kt = kt < nk ? kt : nk - 1;
-        const int k0 = kbase + kt * BK;
-#pragma unroll
-        for (int i = 0; i < LA; ++i) {
-            const int gm = min(m0 + lr + 32 * i, M - 1);
-            r[i] = *reinterpret_cast<const u32x4_t*>(A + (size_t)gm * lda + k0 + lc * 8);
-        }
-#pragma unroll
-        for (int i = 0; i < LB; ++i)
-            r[LA + i] = *reinterpret_cast<const u32x4_t*>(W + (size_t)(n0 + lr + 32 * i) * K + k0 + lc * 8);
-    };
-    auto sstore = [&](const u32x4_t* r, int buf) {
-#pragma unroll
-        for (int i = 0; i < LA; ++i) {
-            const int row = lr + 32 * i;
-            *reinterpret_cast<u32x4_t*>(&As[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[i];
-        }
-#pragma unroll
-        for (int i = 0; i < LB; ++i) {
-            const int row = lr + 32 * i;
-            *reinterpret_cast<u32x4_t*>(&Bs[buf][row * BK + ((lc ^ (row & 7)) << 3)]) = r[LA + i];
-        }
-    };
 
     f32x4_t acc[TM][TN];
 #pragma unroll
@@ -236,7 +240,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    auto compute = [&](int buf) {
+    auto compute = [&](const uint16_t* As) {
+        const uint16_t* Bs = As + BM * BK;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             const int ch = kk * 4 + (lane >> 4);
@@ -244,12 +249,12 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int r = wm * WM + i * 16 + (lane & 15);
-                af[i] = *reinterpret_cast<const bf16x8_t*>(&As[buf][r * BK + ((ch ^ (r & 7)) << 3)]);
+                af[i] = *reinterpret_cast<const bf16x8_t*>(&As[r * BK + ((ch ^ (r & 7)) << 3)]);
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int r = wn * WN + j * 16 + (lane & 15);
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][r * BK + ((ch ^ (r & 7)) << 3)]);
+                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[r * BK + ((ch ^ (r & 7)) << 3)]);
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -273,40 +278,131 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
         for (int v = 0; v < 4; ++v)
             rinfo[i][v] = epi.row_info(min(m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v, M - 1));
-    // tile kt lives in register stage kt % NS
+    auto prefetch_aux = [&]() {
+        if (kPrefetchAux) {
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) gload(R[s], s);
-    if (kPrefetchAux) {
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+                for (int v = 0; v < 4; ++v)
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
-    }
-    sstore(R[0], 0);
-    __syncthreads();
-    // steady state: step kt loads tile kt+NS-1 into the stage tile kt-1 left,
-    // computes tile kt and moves tile kt+1 from registers to the other buffer
-    const int nk_main = nk - nk % NS;
-    for (int kt0 = 0; kt0 < nk_main; kt0 += NS) {
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const int kt = kt0 + s;
-            gload(R[(s + NS - 1) % NS], kt + NS - 1);
-            compute(kt & 1);
-            sstore(R[(s + 1) % NS], (kt + 1) & 1);
-            __syncthreads();
+                    for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
         }
-    }
-    // the last nk % NS steps: their tiles were loaded by the steady loop
+    };
+
+    if constexpr (kDirect) {
+        static_assert(NS >= 2 && NS <= 5, "direct staging depth");
+        constexpr int LPT = LA + LB;   // loads per thread per tile
+        // wavefront wv fills 8-row blocks wv, wv + 4, ... of each operand; lane
+        // l writes row l / 8 of the block at position l % 8
+        const int rr = lane >> 3;
+        const int cg = (lane & 7) ^ rr;   // global chunk stored at position l % 8
+        const uint16_t* asrc[LA];
+        const uint16_t* bsrc[LB];
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) {
-        const int kt = nk_main + s;
-        if (kt < nk) {
-            compute(kt & 1);
-            if (kt + 1 < nk) sstore(R[(s + 1) % NS], (kt + 1) & 1);
-            __syncthreads();
+        for (int i = 0; i < LA; ++i)
+            asrc[i] = A + (size_t)min(m0 + 8 * (i * 4 + wv) + rr, M - 1) * lda + kbase + cg * 8;
+#pragma unroll
+        for (int i = 0; i < LB; ++i)
+            bsrc[i] = W + (size_t)(n0 + 8 * (i * 4 + wv) + rr) * K + kbase + cg * 8;
+        auto issue = [&](int kt, int st) {
+            uint16_t* sb = S + st * STAGE;
+#pragma unroll
+            for (int i = 0; i < LA; ++i) load_to_lds16(asrc[i] + kt * BK, sb + (i * 4 + wv) * 8 * BK);
+#pragma unroll
+            for (int i = 0; i < LB; ++i)
+                load_to_lds16(bsrc[i] + kt * BK, sb + BM * BK + (i * 4 + wv) * 8 * BK);
+        };
+        // tiles 0..NS-2 into stages 0..NS-2 (a launch with fewer steps re-reads
+        // its last tile, so the wait counts below still hold)
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s) issue(s < nk ? s : nk - 1, s);
+        prefetch_aux();
+        // steady steps issue one tile each, NS-1 ahead, into the stage the
+        // previous step read
+        const int steady = nk > NS - 1 ? nk - (NS - 1) : 0;
+        int st = 0;
+        for (int kt = 0; kt < steady; ++kt) {
+            wait_loads<(NS - 2) * LPT>();
+            lds_barrier();
+            issue(kt + NS - 1, st == 0 ? NS - 1 : st - 1);
+            compute(S + st * STAGE);
+            st = st == NS - 1 ? 0 : st + 1;
+        }
+        // the last min(nk, NS-1) steps load nothing; j tiles are younger than
+        // step nk-1-j's (none when the prologue re-read the last tile)
+#pragma unroll
+        for (int j = NS - 2; j >= 0; --j) {
+            if (nk - 1 - j >= steady) {
+                if (nk >= NS - 1 && j > 0) {
+                    if constexpr (NS >= 5) { if (j == 3) wait_loads<3 * LPT>(); }
+                    if constexpr (NS >= 4) { if (j == 2) wait_loads<2 * LPT>(); }
+                    if (j == 1) wait_loads<LPT>();
+                } else {
+                    wait_loads<0>();
+                }
+                lds_barrier();
+                compute(S + st * STAGE);
+                st = st == NS - 1 ? 0 : st + 1;
+            }
+        }
+    } else {
+        const int lc = t & 7, lr = t >> 3;
+        u32x4_t R[NS][LA + LB];
+        auto gload = [&](u32x4_t* r, int kt) {
+            kt = kt < nk ? kt : nk - 1;
+            const int k0 = kbase + kt * BK;
+#pragma unroll
+            for (int i = 0; i < LA; ++i) {
+                const int gm = min(m0 + lr + 32 * i, M - 1);
+                r[i] = *reinterpret_cast<const u32x4_t*>(A + (size_t)gm * lda + k0 + lc * 8);
+            }
+#pragma unroll
+            for (int i = 0; i < LB; ++i)
+                r[LA + i] =
+                    *reinterpret_cast<const u32x4_t*>(W + (size_t)(n0 + lr + 32 * i) * K + k0 + lc * 8);
+        };
+        auto sstore = [&](const u32x4_t* r, int buf) {
+            uint16_t* As = S + buf * STAGE;
+            uint16_t* Bs = As + BM * BK;
+#pragma unroll
+            for (int i = 0; i < LA; ++i) {
+                const int row = lr + 32 * i;
+                *reinterpret_cast<u32x4_t*>(&As[row * BK + ((lc ^ (row & 7)) << 3)]) = r[i];
+            }
+#pragma unroll
+            for (int i = 0; i < LB; ++i) {
+                const int row = lr + 32 * i;
+                *reinterpret_cast<u32x4_t*>(&Bs[row * BK + ((lc ^ (row & 7)) << 3)]) = r[LA + i];
+            }
+        };
+        // tile kt lives in register stage kt % NS
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s) gload(R[s], s);
+        prefetch_aux();
+        sstore(R[0], 0);
+        __syncthreads();
+        // steady state: step kt loads tile kt+NS-1 into the stage tile kt-1 left,
+        // computes tile kt and moves tile kt+1 from registers to the other buffer
+        const int nk_main = nk - nk % NS;
+        for (int kt0 = 0; kt0 < nk_main; kt0 += NS) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const int kt = kt0 + s;
+                gload(R[(s + NS - 1) % NS], kt + NS - 1);
+                compute(S + (kt & 1) * STAGE);
+                sstore(R[(s + 1) % NS], (kt + 1) & 1);
+                __syncthreads();
+            }
+        }
+        // the last nk % NS steps: their tiles were loaded by the steady loop
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s) {
+            const int kt = nk_main + s;
+            if (kt < nk) {
+                compute(S + (kt & 1) * STAGE);
+                if (kt + 1 < nk) sstore(R[(s + 1) % NS], (kt + 1) & 1);
+                __syncthreads();
+            }
         }
     }
 
@@ -356,11 +452,21 @@ static void launch_bf16(const void* A, int lda, const void* W, int N, int K, con
     if (m_cap <= 0) return;
     const int tiles = ((m_cap + BM - 1) / BM) * (N / BN) * splits;
     const int grid = ((tiles + 7) / 8) * 8;
-    // deep register staging for the small tiles of the weight-streaming rounds;
-    // the large tiles have enough MFMA work per step to cover a shallower pipeline
-    constexpr int NS = BM * BN >= 128 * 128 ? 3 : 4;
-    launch(k_gemm_bf16<BM, BN, WGM, WGN, NS, Epi>, dim3(grid), dim3(256), 0, s,
-           (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+    if constexpr (BM * BN >= 128 * 128) {
+        // the large tiles have enough MFMA work per step to cover a shallow
+        // register pipeline (direct staging measured no faster there)
+        launch(k_gemm_bf16<BM, BN, WGM, WGN, 3, false, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+    } else if (tiles <= 512) {
+        // direct staging, 4 stages (64 KB of LDS): two workgroups per CU hold
+        // the whole launch
+        launch(k_gemm_bf16<BM, BN, WGM, WGN, 4, true, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+    } else {
+        // more tiles than two per CU: 3 stages (48 KB), three workgroups per CU
+        launch(k_gemm_bf16<BM, BN, WGM, WGN, 3, true, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+    }
 }
 
 // tile choice by the launch's row cap (the same for Full and Compact rounds):
