@@ -196,12 +196,12 @@ def main() -> int:
     # unless one is given; rollouts below pass gamma = -1 to use the context's
     gamma = args.gamma if args.gamma >= 0 else ctx.hbsjd_calibrate_gamma(B, wl.window)
 
-    def step(seed):
+    def step(seed, counts=out_counts):
         return ctx.hbsjd_rollout(prefix, batch.prefix_len, batch.labels, batch.temperature,
                                  wl.window, history=wl.history, top_k=wl.top_k,
                                  cfg_scale=wl.cfg_scale, seed=seed, exec_mode=mode,
                                  gamma=args.gamma, max_rounds=max_rounds, out_tokens=out_tokens,
-                                 out_counts=out_counts)
+                                 out_counts=counts)
 
     # warm-up; the first warm-up rollout also times every kernel class to find
     # the dominant one
@@ -215,14 +215,18 @@ def main() -> int:
             ctx.hbsjd_profile_start(())
             dominant = max(prof, key=lambda k: prof[k][0])
     torch.cuda.synchronize()
-    # timed region: only the dominant class is bracketed by events
+    # timed region: only the dominant class is bracketed by events. Each timed
+    # rollout writes its own commit counts (allocated here, outside the timed
+    # region): the roofline's algorithmic work is computed from them after the
+    # baseline and ablation runs have reused the shared buffers.
+    timed_counts = [torch.empty_like(out_counts) for _ in range(args.steps)]
     ctx.hbsjd_profile_start([dominant])
     results = []
     step_s = []   # each rollout call is blocking, so the host clock brackets it
     t0 = time.perf_counter()
     for i in range(args.steps):
         ts = time.perf_counter()
-        results.append(step(1000 + i))
+        results.append(step(1000 + i, timed_counts[i]))
         step_s.append(time.perf_counter() - ts)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
