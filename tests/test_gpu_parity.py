@@ -138,6 +138,25 @@ def test_forward_bf16_llamagen_xl_mean_error():
     _bf16_forward_case("llamagen_xl_cfg", [40, 0], 3, atol_max=6e-2)
 
 
+@pytest.mark.parametrize("d,f", [(64, 64), (128, 320), (192, 256)])
+def test_forward_bf16_short_contractions_match_oracle(d, f):
+    """Contractions of 1 to 5 64-deep K steps (K = d, f): fewer steps than the
+    GEMM keeps in flight, exactly as many, and a few more."""
+    shape = synth.small_shape(n_layers=2, d_model=d, n_heads=d // 64, mlp_hidden=f, vocab=1024,
+                              n_classes=10, grid=8)
+    blob = synth.make_weights(shape, 0, std=0.03)
+    ctx = gu.make_ctx(shape, "bf16", blob)
+    om = oracle.Model(shape, gu.bf16_rounded_blob(shape, blob))
+    rng = np.random.default_rng(d)
+    lens = [0, 5, 40, 63, 17]
+    toks = rng.integers(0, shape.vocab, size=(len(lens), shape.T)).astype(np.int32)
+    labels = rng.integers(0, shape.n_classes + 1, size=len(lens)).astype(np.int32)
+    got = ctx.hbsjd_forward(torch.from_numpy(toks).cuda(), lens, labels).cpu().numpy()
+    ref = np.concatenate(om.forward_batch(labels, [toks[i, :n] for i, n in enumerate(lens)]))
+    err = np.abs(got.astype(np.float64) - ref)
+    assert err.max() <= 3e-2 and err.mean() <= 1e-2, (err.max(), err.mean())
+
+
 # ------------------------------------------------------------------ rollouts
 
 
