@@ -173,9 +173,10 @@ struct EpiLogits {
 // the register path's steps past the end re-read the last K tile. The
 // epilogue's own inputs (row metadata, RoPE tables, bias) are fetched before
 // the main loop so their latency hides behind it.
-// With splits > 1 the K range is cut into equal contiguous parts and each part
-// writes fp32 partial sums to `part` ([split][M][N]) instead of calling the
-// epilogue; the caller's reduce kernel adds the parts in split order.
+// When `part` is given the K range is cut into `splits` equal contiguous parts
+// (one part with splits = 1) and each writes fp32 partial sums to `part`
+// ([split][M][N]) instead of calling the epilogue; the caller's reduce kernel
+// adds the parts in split order.
 // An epilogue may opt out of fetching its per-element inputs before the main
 // loop (static constexpr bool kLateAux = true): they are then fetched after it,
 // which frees their registers during the loop at the cost of one exposed load.
@@ -407,7 +408,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
     }
 
     // 16x16 accumulator layout: lane holds rows 4*(lane/16)+v of column lane%16
-    if (splits > 1) {
+    if (part) {
         float* P = part + (size_t)z * m_cap * N;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
