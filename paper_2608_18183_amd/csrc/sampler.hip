@@ -150,7 +150,9 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
         const int v = v0 + k;
         const float l = y[k];
         const float yy = l / tau;
-        y[k] = yy;
+        // entries past V become NaN, which every range test and the softmax's
+        // threshold test below reject
+        y[k] = v < V ? yy : __builtin_nanf("");
         if (v < V) {
             if (l != l) nan_seen = 1;
             if (l > lmax) { lmax = l; lidx = v; }
@@ -193,11 +195,17 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
             for (int k = t; k < kBins; k += 256) hist[k] = 0;
             __syncthreads();
             const float scale = (float)kBins / (hi - lo);
+            // each pass over the entries takes its own copies of the range,
+            // which the compiler cannot see through: otherwise it keeps the 64
+            // range tests of one pass alive for the next ones (128 SGPRs,
+            // spilled to VGPRs)
+            float lo_h = lo, hi_h = hi, scale_h = scale;
+            asm volatile("" : "+v"(lo_h), "+v"(hi_h), "+v"(scale_h));
 #pragma unroll
             for (int k = 0; k < kChunk; ++k) {
                 const float yy = y[k];
-                if (v0 + k < V && yy >= lo && yy <= hi) {
-                    int bin = (int)((yy - lo) * scale);
+                if (yy >= lo_h && yy <= hi_h) {
+                    int bin = (int)((yy - lo_h) * scale_h);
                     bin = bin > kBins - 1 ? kBins - 1 : bin;
                     atomicAdd(&hist[bin], 1);
                 }
@@ -257,10 +265,12 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
             if (cnt <= kCand) {
                 if (t == 0) s_int[3] = 0;
                 __syncthreads();
+                float lo_c = lo, hi_c = hi;
+                asm volatile("" : "+v"(lo_c), "+v"(hi_c));
 #pragma unroll
                 for (int k = 0; k < kChunk; ++k) {
                     const float yy = y[k];
-                    if (v0 + k < V && yy >= lo && yy <= hi) {
+                    if (yy >= lo_c && yy <= hi_c) {
                         int bin = (int)((yy - lo_b) * scale_b);
                         bin = bin > kBins - 1 ? kBins - 1 : bin;
                         if (bin == bstar) cand[atomicAdd(&s_int[3], 1)] = yy;
@@ -282,20 +292,34 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
                 break;
             }
             // narrow to the values that fell into the chosen bin: their exact
-            // minimum and maximum, through LDS atomics on an order-preserving
-            // integer image of the float (a register min/max chain over the 64
-            // entries is turned into a tree that costs ~50 registers)
+            // minimum and maximum, on an order-preserving integer image of the
+            // float: per thread (chains cut every 8 entries, so the compiler
+            // does not rebalance them into trees), per wavefront, then across
+            // the block through LDS atomics. The images are formed from a
+            // copy of the entries the compiler cannot see through, so it does
+            // not hoist all 64 of them out of the search loop
+            {
+                float lo_n = lo, hi_n = hi;
+                int zero = 0;
+                asm volatile("" : "+v"(lo_n), "+v"(hi_n), "+v"(zero));
+                int mn = 0x7fffffff, mx = (int)0x80000000;
 #pragma unroll
-            for (int k = 0; k < kChunk; ++k) {
-                const float yy = y[k];
-                if (v0 + k < V && yy >= lo && yy <= hi) {
+                for (int k = 0; k < kChunk; ++k) {
+                    if ((k & 7) == 0) asm volatile("" : "+v"(mn), "+v"(mx));
+                    const float yy = y[k];
                     int bin = (int)((yy - lo_b) * scale_b);
                     bin = bin > kBins - 1 ? kBins - 1 : bin;
-                    if (bin == bstar) {
-                        const int key = float_key(yy);
-                        atomicMin(&s_mm[0], key);
-                        atomicMax(&s_mm[1], key);
-                    }
+                    const bool sel = yy >= lo_n && yy <= hi_n && bin == bstar;
+                    const int bits = __float_as_int(yy) | zero;
+                    const int key = bits >= 0 ? bits : bits ^ 0x7fffffff;
+                    mn = sel && key < mn ? key : mn;
+                    mx = sel && key > mx ? key : mx;
+                }
+                mn = wave_min_int(mn);
+                mx = wave_max_int(mx);
+                if ((t & 63) == 0) {
+                    atomicMin(&s_mm[0], mn);
+                    atomicMax(&s_mm[1], mx);
                 }
             }
             __syncthreads();
@@ -311,7 +335,7 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     float csum = 0.f;
 #pragma unroll
     for (int k = 0; k < kChunk; ++k) {
-        const float e = (v0 + k < V && y[k] >= thr) ? expf(y[k] - ymax) : 0.f;
+        const float e = (y[k] >= thr) ? expf(y[k] - ymax) : 0.f;
         y[k] = e;
         csum = csum + e;
     }
