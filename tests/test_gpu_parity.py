@@ -138,16 +138,18 @@ def test_forward_bf16_llamagen_xl_mean_error():
     _bf16_forward_case("llamagen_xl_cfg", [40, 0], 3, atol_max=6e-2)
 
 
-def test_forward_bf16_many_rows_matches_oracle():
-    """A forward of ~3000 rows: enough tiles that the O and W2 projections run
-    without a K split (and the other GEMMs on their large-launch variants);
-    sampled sequences against the oracle."""
+@pytest.mark.parametrize("n_seq", [12, 44])
+def test_forward_bf16_many_rows_matches_oracle(n_seq):
+    """Forwards of ~3000 and ~11000 rows: enough tiles that the O and W2
+    projections run without a K split, on the 64x64 tile and then on the
+    128x128 one (and the other GEMMs on their large-launch variants); sampled
+    sequences against the oracle."""
     wl = synth.WORKLOADS["llamagen_b"]
     shape = wl.model
     blob = synth.make_weights(shape, 0, std=wl.weight_std)
     ctx = gu.make_ctx(shape, "bf16", blob)
     rng = np.random.default_rng(21)
-    lens = np.full(12, shape.T - 1, dtype=np.int32)
+    lens = np.full(n_seq, shape.T - 1, dtype=np.int32)
     lens[0], lens[5] = 3, 200
     toks = rng.integers(0, shape.vocab, size=(len(lens), shape.T)).astype(np.int32)
     labels = rng.integers(0, shape.n_classes + 1, size=len(lens)).astype(np.int32)
@@ -155,7 +157,7 @@ def test_forward_bf16_many_rows_matches_oracle():
     row0 = np.concatenate([[0], np.cumsum(lens + 1)])
     assert got.shape == (row0[-1], shape.vocab)
     om = oracle.Model(shape, gu.bf16_rounded_blob(shape, blob))
-    pick = [0, 5, 11]
+    pick = [0, 5, n_seq - 1]
     ref = om.forward_batch(labels[pick], [toks[i, :lens[i]] for i in pick])
     for i, r in zip(pick, ref):
         err = np.abs(got[row0[i]:row0[i + 1]].astype(np.float64) - r)
