@@ -317,6 +317,17 @@ typedef enum hbsjd_kernel {
 hbsjd_status hbsjd_profile_start(hbsjd_ctx* ctx, uint32_t class_mask);
 
 /*
+ * Time one launch in `every` of each timed class. hbsjd_profile_start counts
+ * each class's launches from zero; launch i is bracketed by events when
+ * i % every == 0 and runs unbracketed otherwise, without the events' queue
+ * cost (a few microseconds per bracketed launch). hbsjd_profile_read then
+ * reports the bracketed launches only. every >= 1 (1, the default, brackets
+ * every launch); EINVAL otherwise. Takes effect at once and lasts until the
+ * next call.
+ */
+hbsjd_status hbsjd_profile_sample(hbsjd_ctx* ctx, int32_t every);
+
+/*
  * Read the accumulated timing (synchronises the stream): host arrays of
  * HBSJD_K_COUNT entries, total milliseconds and launch counts per class; either
  * may be NULL.

@@ -68,6 +68,7 @@ _SIGS = {
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
     "hbsjd_profile_start": (_I32, [_P, ctypes.c_uint32]),
+    "hbsjd_profile_sample": (_I32, [_P, ctypes.c_int32]),
     "hbsjd_profile_read": (_I32, [_P, _P, _P]),
     "hbsjd_destroy": (None, [_P]),
     "hbsjd_last_error": (ctypes.c_char_p, []),
@@ -283,6 +284,9 @@ class Context:
         for k in classes:
             mask |= 1 << KERNELS.index(k)
         _check(self._lib.hbsjd_profile_start(self._h, mask), "hbsjd_profile_start")
+
+    def hbsjd_profile_sample(self, every: int = 1):
+        _check(self._lib.hbsjd_profile_sample(self._h, int(every)), "hbsjd_profile_sample")
 
     def hbsjd_profile_read(self) -> dict:
         ms = np.zeros(len(KERNELS), dtype=np.float64)

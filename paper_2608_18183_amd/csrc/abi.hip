@@ -106,6 +106,8 @@ struct hbsjd_ctx {
 
     // per-kernel-class timing (hbsjd_profile_start / hbsjd_profile_read)
     uint32_t prof_mask = 0;
+    int32_t prof_every = 1;                  // one bracketed launch in prof_every
+    int64_t prof_seen[HBSJD_K_COUNT] = {};   // launches of each class since profile_start
     std::vector<hipEvent_t> prof_free;
     std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> prof_pending;
     double prof_ms[HBSJD_K_COUNT] = {};
@@ -225,7 +227,7 @@ struct Timed {
     int cls;
     bool armed = false;
     Timed(hbsjd_ctx* ctx, int k) : c(ctx), cls(k) {
-        if (c->prof_mask & (1u << k)) {
+        if ((c->prof_mask & (1u << k)) && c->prof_seen[k]++ % c->prof_every == 0) {
             LaunchEvents* ev = launch_events();
             ev->start = prof_event(c);
             ev->stop = prof_event(c);
@@ -1314,11 +1316,23 @@ hbsjd_status hbsjd_profile_start(hbsjd_ctx* c, uint32_t class_mask) {
         for (int k = 0; k < HBSJD_K_COUNT; ++k) {
             c->prof_ms[k] = 0.0;
             c->prof_n[k] = 0;
+            c->prof_seen[k] = 0;
         }
         c->prof_mask = class_mask & ((1u << HBSJD_K_COUNT) - 1);
         return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_profile_start");
+    }
+}
+
+hbsjd_status hbsjd_profile_sample(hbsjd_ctx* c, int32_t every) {
+    try {
+        GUARD(c);
+        if (every < 1) return fail(HBSJD_EINVAL, "profile sample interval must be >= 1");
+        c->prof_every = every;
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_profile_sample");
     }
 }
 

@@ -536,3 +536,38 @@ def test_calibrate_gamma_drives_auto_mode(tiny, dtype):
     ref = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
                             batch.temperature, W, seed=5, exec_mode=P().EXEC_FULL)
     assert np.array_equal(out["tokens"].cpu().numpy(), ref["tokens"].cpu().numpy())
+
+
+# ------------------------------------------------------------------ kernel timing
+
+
+def test_profile_sampling_brackets_one_launch_in_every(tiny):
+    """Per-class timing brackets one launch in `every` of each timed class and
+    changes no result."""
+    w, blob, _ = tiny
+    ctx = gu.make_ctx(w.model, "f32", blob)
+    batch = synth.make_batch(w, 3)
+
+    def run():
+        return ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                                 batch.temperature, w.window, history=w.history, seed=5)
+
+    base = run()["tokens"].cpu().numpy()
+    counts = {}
+    for every in (1, 3):
+        ctx.hbsjd_profile_sample(every)
+        ctx.hbsjd_profile_start(["qkv", "verify"])
+        out = run()
+        prof = ctx.hbsjd_profile_read()
+        ctx.hbsjd_profile_start(())
+        assert np.array_equal(out["tokens"].cpu().numpy(), base)
+        assert prof["qkv"][0] > 0 and prof["verify"][0] > 0
+        assert prof["attn"] == (0.0, 0)
+        counts[every] = (prof["qkv"][1], prof["verify"][1])
+    ctx.hbsjd_profile_sample(1)
+    for n1, n3 in zip(counts[1], counts[3]):
+        assert n1 > 3 and -(-n1 // 3) - 1 <= n3 <= -(-n1 // 3), counts
+    for bad in (0, -2):
+        with pytest.raises(P().HbsjdError) as ei:
+            ctx.hbsjd_profile_sample(bad)
+        assert ei.value.code == "EINVAL"
