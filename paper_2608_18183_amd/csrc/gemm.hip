@@ -6,9 +6,11 @@
 // bf16 path: 256-thread workgroups, 2x2 wavefronts, LDS-staged 64-deep K
 // tiles with an XOR swizzle (loaded straight into LDS for the 64x64 tile,
 // through registers for the 128x128 one), v_mfma_f32_16x16x32_bf16 with fp32
-// accumulation. Every output element sums its K range in the same order no
-// matter how many rows the launch has or where the row sits, so a row's result
-// does not depend on the rest of the batch.
+// accumulation. An output element sums its K range in the same order wherever
+// its row sits in the launch, and for the unsplit projections (QKV, W1|W3,
+// lm_head) whatever the launch's size or tile. O and W2 cut K into as many
+// parts as split_for gives for the launch's row capacity, so there the order
+// of the partial sums, and a row's last bits, follow that capacity.
 // fp32 path: a plain LDS-tiled FMA kernel for the exact-parity mode.
 #include "common.h"
 #include "launch.h"

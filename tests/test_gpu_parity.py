@@ -317,7 +317,9 @@ def test_rollout_ar_f32_cfg_equals_oracle_ar():
 
 def test_rollout_ar_bf16_equals_sjd_window_1():
     # W = 1 SJD accepts every draft (its proposal is the same row recomputed),
-    # so it must reproduce the AR baseline token for token on the GPU as well
+    # so it reproduces the AR baseline token for token on the GPU as well, as
+    # long as the row at position k_b (SJD prefill, first AR round) sees the
+    # same K split of O and W2 in both launches: 4 parts at these prefixes
     wl = synth.WORKLOADS["llamagen_b"]
     shape = wl.model
     blob = synth.make_weights(shape, 0)
