@@ -70,19 +70,58 @@ struct EpiQkv {
         const int pi = part < 2 ? ri.p * (dhv >> 1) + (e >> 1) : 0;
         return Aux{rc[pi], rs[pi]};
     }
+    // element n of a row after RoPE: q and k pairs (2i, 2i+1) turned by the
+    // row/column angle of the row's position; v as is
+    __device__ float value(const Aux& ax, int n, float v, float partner) const {
+        if (part == 2) return v;
+        const int dhv = head_dim();
+        const int c = n - part * d;
+        const int e = kDh ? c & (kDh - 1) : c % dhv;
+        return (e & 1) ? (partner * ax.sn + v * ax.cs) : (v * ax.cs - partner * ax.sn);
+    }
     __device__ void store(const Row& ri, const Aux& ax, int m, int n, float v, float partner) const {
         const int dhv = head_dim();
         const int c = n - part * d;
         const int head = kDh ? c / kDh : c / dhv;
         const int e = c - head * dhv;
-        float out = v;
-        if (part < 2) {
-            const float cs = ax.cs, sn = ax.sn;
-            // adjacent pair (2i, 2i+1) turned by the row/column angle of position p
-            out = (e & 1) ? (partner * sn + v * cs) : (v * cs - partner * sn);
-        }
+        const float out = value(ax, n, v, partner);
         const int col = part == 0 ? c : part == 1 ? head * 64 * dhv + e : head * 64 * dhv + e * 64;
         Elem<T>::store((part == 0 ? q : kv) + (ri.off + col), out);
+    }
+    // bf16 64x64 tiles (one head of one part) are staged in LDS as bf16,
+    // tile[r * tile_ld() + c], and written from there: q and K rows as eight
+    // 16-byte chunks per row, V^T one row (= cache slot) per lane, so a
+    // wavefront's store covers consecutive slots of one dimension instead of
+    // 16 dimensions of 4 rows
+    static constexpr bool kTileStore = sizeof(T) == 2;
+    __device__ int tile_ld() const { return part == 2 ? 66 : 72; }   // 16-byte rows; odd dwords
+    __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
+        const int t = threadIdx.x, ld = tile_ld();
+        const int c0 = n0 - part * d;   // first column of the tile in its part
+        const int head = c0 >> 6;
+        if (part < 2) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int qd = t + 256 * h, r = qd >> 3, ch = qd & 7, m = m0 + r;
+                if (m < M) {
+                    const Row ri = row_info(m);
+                    T* dst = (part == 0 ? q + ri.off + c0 : kv + ri.off + head * 64 * 64) + ch * 8;
+                    *reinterpret_cast<u32x4_t*>(dst) =
+                        *reinterpret_cast<const u32x4_t*>(tile + r * ld + ch * 8);
+                }
+            }
+        } else {
+            const int r = t & 63, m = m0 + r;
+            if (m < M) {
+                const Row ri = row_info(m);
+                T* dst = kv + ri.off + head * 64 * 64;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    const int e = (t >> 6) + 4 * k;
+                    dst[e * 64] = tile[r * ld + e];
+                }
+            }
+        }
     }
     __device__ void operator()(int m, int n, float v, float partner) const {
         EpiQkv e = *this;
@@ -186,6 +225,12 @@ template <typename E>
 constexpr auto epi_prefetches_aux(int) -> decltype(E::kLateAux, bool()) { return !E::kLateAux; }
 template <typename E>
 constexpr bool epi_prefetches_aux(long) { return true; }
+// an epilogue may stage a 64x64 bf16 tile in LDS and store it itself
+// (static constexpr bool kTileStore = true; value() and store_tile())
+template <typename E>
+constexpr auto epi_stores_tile(int) -> decltype(E::kTileStore, bool()) { return E::kTileStore; }
+template <typename E>
+constexpr bool epi_stores_tile(long) { return false; }
 
 // one 16-byte chunk per lane from global memory to LDS: lane l's chunk lands
 // at lds + 16 l (lds is the same for the whole wavefront)
@@ -430,6 +475,28 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
             for (int v = 0; v < 4; ++v)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
+    }
+    if constexpr (epi_stores_tile<Epi>(0) && BM == 64 && BN == 64) {
+        __syncthreads();   // every wavefront is done with the operand stages
+        uint16_t* tile = S;
+        const int ld = epi.tile_ld();
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int rl = wm * WM + i * 16 + 4 * (lane >> 4) + v;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const float val = acc[i][j][v];
+                    const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
+                        0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
+                    tile[rl * ld + wn * WN + j * 16 + (lane & 15)] =
+                        f32_to_bf16_rne(epi.value(aux[i][v][j], col0 + j * 16, val, partner));
+                }
+            }
+        __syncthreads();
+        epi.store_tile(tile, n0, m0, M);
+        return;
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
