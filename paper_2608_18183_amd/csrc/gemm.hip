@@ -95,6 +95,11 @@ struct EpiQkv {
     // 16 dimensions of 4 rows
     static constexpr bool kTileStore = sizeof(T) == 2;
     __device__ int tile_ld() const { return part == 2 ? 66 : 72; }   // 16-byte rows; odd dwords
+    // element (rl, cl) of the tile (local row and column), global column n
+    __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux& ax, int n, float v,
+                          float partner) const {
+        tile[rl * ld + cl] = f32_to_bf16_rne(value(ax, n, v, partner));
+    }
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
         const int t = threadIdx.x, ld = tile_ld();
         const int c0 = n0 - part * d;   // first column of the tile in its part
@@ -159,10 +164,26 @@ struct EpiSwiGLU {
     __device__ Row row_info(int) const { return Row{}; }
     __device__ Aux aux(const Row&, int) const { return Aux{}; }
     // columns 2i / 2i+1 are the gate (W1 row i) and the up projection (W3 row i)
+    __device__ static float swiglu(float gate, float up) {
+        return gate / (1.0f + __expf(-gate)) * up;
+    }
     __device__ void store(const Row&, const Aux&, int m, int n, float v, float partner) const {
         if (n & 1) return;
-        const float silu = v / (1.0f + __expf(-v));
-        Elem<T>::store(act + (size_t)m * ld + (n >> 1), silu * partner);
+        Elem<T>::store(act + (size_t)m * ld + (n >> 1), swiglu(v, partner));
+    }
+    // bf16 64x64 tiles give 64 rows of 32 outputs, staged in LDS and written as
+    // four 16-byte chunks per row
+    static constexpr bool kTileStore = sizeof(T) == 2;
+    __device__ int tile_ld() const { return 40; }
+    __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux&, int, float v,
+                          float partner) const {
+        if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_bf16_rne(swiglu(v, partner));
+    }
+    __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
+        const int t = threadIdx.x, r = t >> 2, ch = t & 3, m = m0 + r;
+        if (m < M)
+            *reinterpret_cast<u32x4_t*>(act + (size_t)m * ld + (n0 >> 1) + ch * 8) =
+                *reinterpret_cast<const u32x4_t*>(tile + r * 40 + ch * 8);
     }
     __device__ void operator()(const Row& r, int m, int n, float v, float p) const {
         store(r, Aux{}, m, n, v, p);
@@ -490,8 +511,8 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
                     const float val = acc[i][j][v];
                     const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
                         0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
-                    tile[rl * ld + wn * WN + j * 16 + (lane & 15)] =
-                        f32_to_bf16_rne(epi.value(aux[i][v][j], col0 + j * 16, val, partner));
+                    epi.stage(tile, ld, rl, wn * WN + j * 16 + (lane & 15), aux[i][v][j],
+                              col0 + j * 16, val, partner);
                 }
             }
         __syncthreads();
