@@ -110,6 +110,45 @@ def rollout_work(cls, shape, prefix_len, counts, W, cfg, esz=2):
     return tot_b, tot_f
 
 
+def path_work(shape, prefix_len, counts, W, cfg, esz=2):
+    """Algorithmic (bytes, flops) of one whole rollout (prefill and every
+    round), from the per-round commit counts (host array [rounds, B]); active
+    images only. Per forward: the weights once; each sequence's KV read once
+    per layer and the new rows' KV written; the logits written and read once
+    and one probability row per image kept as the next round's proposal.
+    Flops: 2 per weight per row (the lm_head on its rows only) plus 4 d per
+    layer, row and key attended."""
+    d, f, V, L, T = shape.d_model, shape.mlp_hidden, shape.vocab, shape.n_layers, shape.T
+    layer_params = L * (4 * d * d + 3 * d * f)
+    wbytes = (layer_params + d * V) * esz
+    kv_row = L * 2 * d * esz            # K and V of one position, all layers
+    k = prefix_len.astype(np.int64)
+    act = k < T
+    ka = k[act]
+    n_img = int(act.sum())
+    # prefill: positions 0..k_b of each active image (both CFG branches); the
+    # lm_head runs on each sequence's last row
+    rows = int(np.sum(ka + 1)) * cfg
+    keys = int(np.sum((ka + 1) * (ka + 2) // 2)) * cfg
+    out_rows = n_img * cfg
+    tot_b = wbytes + 2 * rows * kv_row + out_rows * V * 8 + n_img * V * 4
+    tot_f = 2.0 * rows * layer_params + 2.0 * out_rows * d * V + 4.0 * d * L * keys
+    cur = k.copy()
+    for r in range(counts.shape[0]):
+        a = cur < T
+        A = int(a.sum())
+        if A == 0:
+            break
+        n = cur[a]
+        rows = A * cfg * (W + 1)
+        keys = int(np.sum((W + 1) * (n + 1) + W * (W + 1) // 2)) * cfg
+        tot_b += (wbytes + int(np.sum(n)) * cfg * kv_row + rows * kv_row + rows * V * 8
+                  + A * V * 4)
+        tot_f += 2.0 * rows * (layer_params + d * V) + 4.0 * d * L * keys
+        cur = cur + counts[r]
+    return tot_b, tot_f
+
+
 def measured_traffic(cls):
     """HBM bytes per launch of a kernel class from the committed counter
     summary (profiles/hbm_traffic.json: FETCH_SIZE and WRITE_SIZE passes scaled
@@ -375,6 +414,20 @@ def main() -> int:
         roof = {"bound": "hbm", "achieved": round(tb / t_s / 1e9, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 5)
+    # the whole path over the timed rollouts (prefill and rounds)
+    pb = pf = 0.0
+    for r in results:
+        b, fl = path_work(shape, batch.prefix_len, r["counts"].cpu().numpy(), wl.window, cfg,
+                          esz=2 if wl.dtype == "bf16" else 4)
+        pb += b
+        pf += fl
+    path = {"bytes_per_step": round(pb / len(results)), "flops_per_step": round(pf / len(results)),
+            "achieved_gbs": round(pb / elapsed / 1e9, 2),
+            "frac_hbm": round(pb / elapsed / 1e9 / HBM_PEAK_GBS, 5),
+            "achieved_tflops": round(pf / elapsed / 1e12, 3),
+            "frac_mfma": round(pf / elapsed / 1e12 / BF16_PEAK_TFLOPS, 5),
+            "bound": "hbm" if pb / (HBM_PEAK_GBS * 1e9) >= pf / (BF16_PEAK_TFLOPS * 1e12)
+            else "mfma"}
     roof["traffic"] = measured_traffic(dominant)
     roof["kernel"] = dominant
     roof["launches"] = dom_n * timed_every
@@ -434,6 +487,7 @@ def main() -> int:
         "reject_rate": round(reject_rate, 4),
         "committed_tokens_per_step": committed_per_step,
         "roofline": roof,
+        "path_roofline": path,
         "cached_ar": ar,
         "ablations": ablations,
         "teacher_scoring": scoring,
