@@ -309,10 +309,11 @@ typedef enum hbsjd_kernel {
 } hbsjd_kernel;
 
 /*
- * Start timing: from now on every launch of the classes whose bit is set in
- * `class_mask` (bit k = hbsjd_kernel k) is bracketed by HIP events on the
- * context's stream; counters restart at zero. class_mask 0 stops timing.
- * Timing adds an event record per launch and does not change results.
+ * Start timing: from now on launches of the classes whose bit is set in
+ * `class_mask` (bit k = hbsjd_kernel k) are bracketed by HIP events on the
+ * context's stream, every launch or one in hbsjd_profile_sample's interval;
+ * counters restart at zero. class_mask 0 stops timing. Timing adds event
+ * records to the bracketed launches and does not change results.
  */
 hbsjd_status hbsjd_profile_start(hbsjd_ctx* ctx, uint32_t class_mask);
 
