@@ -88,42 +88,47 @@ struct EpiQkv {
         const int col = part == 0 ? c : part == 1 ? head * 64 * dhv + e : head * 64 * dhv + e * 64;
         Elem<T>::store((part == 0 ? q : kv) + (ri.off + col), out);
     }
-    // bf16 64x64 tiles (one head of one part) are staged in LDS as bf16,
-    // tile[r * tile_ld() + c], and written from there: q and K rows as eight
-    // 16-byte chunks per row, V^T one row (= cache slot) per lane, so a
-    // wavefront's store covers consecutive slots of one dimension instead of
-    // 16 dimensions of 4 rows
-    static constexpr bool kTileStore = sizeof(T) == 2;
-    __device__ int tile_ld() const { return part == 2 ? 66 : 72; }   // 16-byte rows; odd dwords
+    // bf16 square tiles of BT = 64 or 128 columns (BT / 64 heads of one part)
+    // are staged in LDS as bf16, tile[r * tile_ld<BT>() + c], and written from
+    // there: q and K rows as 16-byte chunks (eight lanes per head row), V^T one
+    // row (= cache slot) per lane, so a wavefront's store covers consecutive
+    // slots of one dimension instead of 16 dimensions of 4 rows
+    static constexpr bool stores_tile(int bt) { return sizeof(T) == 2 && (bt == 64 || bt == 128); }
+    template <int BT>
+    __device__ int tile_ld() const { return part == 2 ? BT + 2 : BT + 8; }   // odd dwords; 16-byte rows
     // element (rl, cl) of the tile (local row and column), global column n
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux& ax, int n, float v,
                           float partner) const {
         tile[rl * ld + cl] = f32_to_bf16_rne(value(ax, n, v, partner));
     }
+    template <int BT>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
-        const int t = threadIdx.x, ld = tile_ld();
+        const int t = threadIdx.x, ld = tile_ld<BT>();
         const int c0 = n0 - part * d;   // first column of the tile in its part
         const int head = c0 >> 6;
         if (part < 2) {
+            constexpr int kChunks = BT / 8;   // 16-byte chunks per row
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int qd = t + 256 * h, r = qd >> 3, ch = qd & 7, m = m0 + r;
+            for (int h = 0; h < BT * kChunks / 256; ++h) {
+                const int qd = t + 256 * h, r = qd / kChunks, col = (qd % kChunks) * 8, m = m0 + r;
                 if (m < M) {
                     const Row ri = row_info(m);
-                    T* dst = (part == 0 ? q + ri.off + c0 : kv + ri.off + head * 64 * 64) + ch * 8;
+                    T* dst = part == 0 ? q + ri.off + c0 + col
+                                       : kv + ri.off + (head + (col >> 6)) * 64 * 64 + (col & 63);
                     *reinterpret_cast<u32x4_t*>(dst) =
-                        *reinterpret_cast<const u32x4_t*>(tile + r * ld + ch * 8);
+                        *reinterpret_cast<const u32x4_t*>(tile + r * ld + col);
                 }
             }
         } else {
-            const int r = t & 63, m = m0 + r;
+            constexpr int kGroups = 256 / BT;   // threads per row, each a strided set of columns
+            const int r = t % BT, m = m0 + r;
             if (m < M) {
                 const Row ri = row_info(m);
                 T* dst = kv + ri.off + head * 64 * 64;
 #pragma unroll
-                for (int k = 0; k < 16; ++k) {
-                    const int e = (t >> 6) + 4 * k;
-                    dst[e * 64] = tile[r * ld + e];
+                for (int k = 0; k < BT / kGroups; ++k) {
+                    const int e = t / BT + kGroups * k;
+                    dst[(e >> 6) * 64 * 64 + (e & 63) * 64] = tile[r * ld + e];
                 }
             }
         }
@@ -171,19 +176,28 @@ struct EpiSwiGLU {
         if (n & 1) return;
         Elem<T>::store(act + (size_t)m * ld + (n >> 1), swiglu(v, partner));
     }
-    // bf16 64x64 tiles give 64 rows of 32 outputs, staged in LDS and written as
-    // four 16-byte chunks per row
-    static constexpr bool kTileStore = sizeof(T) == 2;
-    __device__ int tile_ld() const { return 40; }
+    // bf16 square tiles of BT columns give BT rows of BT / 2 outputs, staged
+    // in LDS and written as 16-byte chunks per row. Only the 64x64 tile uses
+    // it: at 128x128 the staging measured slower than storing from registers
+    // (stress rounds 48 -> 53 us per launch)
+    static constexpr bool stores_tile(int bt) { return sizeof(T) == 2 && bt == 64; }
+    template <int BT>
+    __device__ int tile_ld() const { return BT / 2 + 8; }
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux&, int, float v,
                           float partner) const {
         if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_bf16_rne(swiglu(v, partner));
     }
+    template <int BT>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
-        const int t = threadIdx.x, r = t >> 2, ch = t & 3, m = m0 + r;
-        if (m < M)
-            *reinterpret_cast<u32x4_t*>(act + (size_t)m * ld + (n0 >> 1) + ch * 8) =
-                *reinterpret_cast<const u32x4_t*>(tile + r * 40 + ch * 8);
+        constexpr int kChunks = BT / 16;   // 16-byte chunks per row of BT / 2 outputs
+        const int t = threadIdx.x, ldt = tile_ld<BT>();
+#pragma unroll
+        for (int h = 0; h < BT * kChunks / 256; ++h) {
+            const int qd = t + 256 * h, r = qd / kChunks, ch = qd % kChunks, m = m0 + r;
+            if (m < M)
+                *reinterpret_cast<u32x4_t*>(act + (size_t)m * ld + (n0 >> 1) + ch * 8) =
+                    *reinterpret_cast<const u32x4_t*>(tile + r * ldt + ch * 8);
+        }
     }
     __device__ void operator()(const Row& r, int m, int n, float v, float p) const {
         store(r, Aux{}, m, n, v, p);
@@ -246,10 +260,12 @@ template <typename E>
 constexpr auto epi_prefetches_aux(int) -> decltype(E::kLateAux, bool()) { return !E::kLateAux; }
 template <typename E>
 constexpr bool epi_prefetches_aux(long) { return true; }
-// an epilogue may stage a 64x64 bf16 tile in LDS and store it itself
-// (static constexpr bool kTileStore = true; value() and store_tile())
+// an epilogue may stage a square bf16 tile in LDS and store it itself
+// (static constexpr bool stores_tile(int tile width); stage(), store_tile())
 template <typename E>
-constexpr auto epi_stores_tile(int) -> decltype(E::kTileStore, bool()) { return E::kTileStore; }
+constexpr auto epi_stores_tile(int bt) -> decltype(E::stores_tile(0), bool()) {
+    return E::stores_tile(bt);
+}
 template <typename E>
 constexpr bool epi_stores_tile(long) { return false; }
 
@@ -497,10 +513,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
                 for (int j = 0; j < TN; ++j) aux[i][v][j] = epi.aux(rinfo[i][v], col0 + j * 16);
     }
-    if constexpr (epi_stores_tile<Epi>(0) && BM == 64 && BN == 64) {
+    if constexpr (BM == BN && epi_stores_tile<Epi>(BN)) {
         __syncthreads();   // every wavefront is done with the operand stages
         uint16_t* tile = S;
-        const int ld = epi.tile_ld();
+        const int ld = epi.template tile_ld<BN>();
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -516,7 +532,7 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
                 }
             }
         __syncthreads();
-        epi.store_tile(tile, n0, m0, M);
+        epi.template store_tile<BN>(tile, n0, m0, M);
         return;
     }
 #pragma unroll
