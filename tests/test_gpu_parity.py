@@ -238,6 +238,32 @@ def test_rollout_f32_cfg_equals_oracle():
     assert np.array_equal(g["counts"].cpu().numpy(), o["counts"])
 
 
+@pytest.mark.parametrize("case", ["single_image", "all_complete", "window_past_end"])
+def test_rollout_f32_edge_cases_equal_oracle(tiny, case):
+    """Degenerate batches against the oracle: one image; every image already
+    complete (no round runs); a window far longer than what is left."""
+    w, blob, om = tiny
+    T = w.model.T
+    if case == "single_image":
+        batch = synth.make_batch(w, 4, batch=1)
+        W = w.window
+    elif case == "all_complete":
+        batch = synth.make_batch(w, 5)
+        batch.prefix_len[:] = T
+        W = w.window
+    else:
+        batch = synth.make_batch(w, 6)
+        batch.prefix_len[:] = [T - 1, T - 3, T - 2, 0]
+        W = 40
+    g, o = _run_both(w, blob, om, batch, 321, W, P().EXEC_AUTO)
+    assert np.array_equal(g["tokens"].cpu().numpy(), o["tokens"])
+    assert g["rounds"] == o["rounds"]
+    assert np.array_equal(g["counts"].cpu().numpy(), o["counts"])
+    if case == "all_complete":
+        assert g["rounds"] == 0
+        assert np.array_equal(g["tokens"].cpu().numpy(), batch.prefix_tokens)
+
+
 def test_rollout_bf16_full_equals_compact_and_counts_are_bounded():
     wl = synth.WORKLOADS["llamagen_b"]
     shape = wl.model
