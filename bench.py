@@ -186,6 +186,45 @@ def cpu_baseline(shape, blob_rounded, batch, wl, n_img, rounds):
     return committed / dt, committed, dt
 
 
+def achievable_peaks() -> int:
+    """What this GPU reaches outside the library, next to the datasheet peaks the
+    roofline uses: a 1 GiB device-to-device copy (bytes read + written per
+    second) and a large bf16 matmul through torch (hipBLASLt)."""
+    import torch
+    torch.cuda.set_device(0)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / 1e3 / reps
+
+    a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    t_copy = timed(lambda: b.copy_(a), 20)
+    copy_gbs = 2 * a.numel() * 4 / t_copy / 1e9
+    del a, b
+    n = 8192
+    x = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    y = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    t_mm = timed(lambda: torch.matmul(x, y), 20)
+    tflops = 2.0 * n ** 3 / t_mm / 1e12
+    print(json.dumps({"achievable_peaks": {
+        "copy_gbs": round(copy_gbs, 1), "copy_frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
+        "copy_bytes": 2 * (1 << 30),
+        "bf16_matmul_tflops": round(tflops, 1),
+        "bf16_matmul_frac_of_peak": round(tflops / BF16_PEAK_TFLOPS, 4),
+        "matmul_shape": [n, n, n], "matmul": "torch.matmul (hipBLASLt)"}}))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -203,7 +242,12 @@ def main() -> int:
     ap.add_argument("--ablation-steps", type=int, default=1,
                     help="timed rollouts per execution ablation: Full, Compact, a gamma sweep "
                          "and Batch-Synchronous SJD (0 = skip)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure achievable peaks instead (a 1 GiB device copy and a "
+                         "8192^3 bf16 torch.matmul) and print them as one JSON line")
     args = ap.parse_args()
+    if args.peaks:
+        return achievable_peaks()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the rollout "
               f"shards by image with no cross-GPU exchange, so each GPU would run its own "
