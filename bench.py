@@ -216,7 +216,16 @@ def achievable_peaks() -> int:
     y = torch.randn(n, n, device="cuda").to(torch.bfloat16)
     t_mm = timed(lambda: torch.matmul(x, y), 20)
     tflops = 2.0 * n ** 3 / t_mm / 1e12
+    del x, y
+    # the XL round's W1|W3 product (8448 rows, K 1280, N 6912), W stored [N][K]
+    m, k, nn = 8448, 1280, 6912
+    xa = torch.randn(m, k, device="cuda").to(torch.bfloat16)
+    wt = torch.randn(nn, k, device="cuda").to(torch.bfloat16).t()
+    t_xl = timed(lambda: torch.matmul(xa, wt), 20)
+    xl_tflops = 2.0 * m * k * nn / t_xl / 1e12
     print(json.dumps({"achievable_peaks": {
+        "xl_w13_matmul_tflops": round(xl_tflops, 1), "xl_w13_matmul_us": round(t_xl * 1e6, 1),
+        "xl_w13_shape_mkn": [m, k, nn],
         "copy_gbs": round(copy_gbs, 1), "copy_frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
         "copy_bytes": 2 * (1 << 30),
         "bf16_matmul_tflops": round(tflops, 1),
