@@ -52,7 +52,7 @@ class _Args(ctypes.Structure):
 
 class _Out(ctypes.Structure):
     _fields_ = [("tokens", _P), ("counts", _P), ("rounds", _P), ("active_hist", _P),
-                ("mode_hist", _P), ("stats", _P)]
+                ("mode_hist", _P), ("stats", _P), ("trace_drafts", _P), ("trace_q", _P)]
 
 
 def lib():
@@ -94,6 +94,8 @@ def set_debug(flags: int) -> None:
 DEBUG_RESIDUAL_DROPS_Q = 1
 DEBUG_INVERTED_RATIO = 2
 DEBUG_ROPE_SIGN = 4
+DEBUG_HISTORY_SHIFT = 8
+DEBUG_REUSE_SHIFT = 16
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
@@ -170,10 +172,15 @@ class Model:
     def rollout(self, batch, W: int, H: int = 24, top_k: int = 0, cfg_scale: float = 0.0,
                 seed: int = 0, greedy: bool = False, exec_mode: int = 2, gamma: int = 0,
                 max_rounds: Optional[int] = None, allow_partial: bool = False,
-                sync: bool = False) -> dict:
+                sync: bool = False, trace: bool = False) -> dict:
         """Batched SJD rollout. exec_mode 0 Full, 1 Compact, 2 Auto (Full iff A > gamma).
         sync=True runs the Batch-Synchronous SJD ablation (shared window
-        boundaries, Sec. 4.2 and Table 2) instead of independent progress."""
+        boundaries, Sec. 4.2 and Table 2) instead of independent progress.
+        trace=True also returns the window after the prefill and after every
+        round: 'trace_drafts' [rounds+1, B, W] (-1 past T or once complete) and
+        'trace_q' [rounds+1, B, W], each draft's proposal probability q(z)
+        (the reused row's p(z); 1 for a history draft and in greedy mode; 0
+        where the draft is -1)."""
         B = len(batch.prefix_len)
         if max_rounds is None:
             max_rounds = int(self.T - np.min(batch.prefix_len)) + 1
@@ -185,14 +192,23 @@ class Model:
         ahist = np.zeros(max_rounds, dtype=np.int32)
         mhist = np.zeros(max_rounds, dtype=np.int32)
         stats = np.zeros(3, dtype=np.int64)
-        o = _Out(_ptr(tokens), _ptr(counts), _ptr(rounds), _ptr(ahist), _ptr(mhist), _ptr(stats))
+        tr_d = tr_q = None
+        if trace:
+            tr_d = np.full((max_rounds + 1, B, W), -1, dtype=np.int32)
+            tr_q = np.zeros((max_rounds + 1, B, W), dtype=np.float32)
+        o = _Out(_ptr(tokens), _ptr(counts), _ptr(rounds), _ptr(ahist), _ptr(mhist), _ptr(stats),
+                 _ptr(tr_d) if trace else None, _ptr(tr_q) if trace else None)
         st = lib().om_rollout(self._h, ctypes.byref(a), ctypes.byref(o))
         if st != 0 and not (st == -2 and allow_partial):
             raise RuntimeError(f"oracle rollout failed with status {st}")
         r = int(rounds[0])
-        return dict(tokens=tokens, counts=counts[:r], rounds=r, active=ahist[:r],
-                    mode=mhist[:r], verified=int(stats[0]), rejected=int(stats[1]),
-                    image_rounds=int(stats[2]), complete=(st == 0))
+        res = dict(tokens=tokens, counts=counts[:r], rounds=r, active=ahist[:r],
+                   mode=mhist[:r], verified=int(stats[0]), rejected=int(stats[1]),
+                   image_rounds=int(stats[2]), complete=(st == 0))
+        if trace:
+            res["trace_drafts"] = tr_d[:r + 1]
+            res["trace_q"] = tr_q[:r + 1]
+        return res
 
     def rollout_ar(self, batch, top_k: int = 0, cfg_scale: float = 0.0, seed: int = 0,
                    greedy: bool = False) -> np.ndarray:

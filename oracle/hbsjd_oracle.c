@@ -54,6 +54,10 @@
  * k_b + wW + 1 .. min(k_b + (w+1)W, T) (each image counts windows from its own
  * prefix); an image waiting at the boundary still forwards its last committed
  * token and re-draws its first draft from that row, committing nothing.
+ *
+ * om_rollout can also record every image's window (drafts and the proposal
+ * probability q(z) of each) after the prefill and after every round, so that
+ * tests can compare the refresh step round by round.
  */
 #include <math.h>
 #include <stdint.h>
@@ -83,6 +87,8 @@ void om_set_debug(int flags) { g_debug = flags; }
 #define DBG_RESIDUAL_DROPS_Q 1
 #define DBG_INVERTED_RATIO 2
 #define DBG_ROPE_SIGN 4
+#define DBG_HISTORY_SHIFT 8   /* history token one position later: S[pos - H + 1] */
+#define DBG_REUSE_SHIFT 16    /* reused prediction taken from the next row */
 
 /* ---------------------------------------------------------------- utils */
 
@@ -551,6 +557,13 @@ typedef struct {
     int* active_hist;   /* [max_rounds] or NULL */
     int* mode_hist;     /* [max_rounds] or NULL: 0 Full, 1 Compact */
     long* stats;        /* [3] or NULL: drafts verified, drafts rejected, image-rounds */
+    /* the window after the prefill (entry 0) and after each round r (entry r+1),
+       or NULL: [max_rounds + 1][B][W] drafts at positions n_b + 1 + m (-1 past T
+       or once the image is complete) and their proposal probability q(z):
+       the reused row's p(z), 1 for a point-mass (history) proposal and in
+       greedy mode, 0 where the draft is -1 */
+    int* trace_drafts;
+    float* trace_q;
 } om_rollout_out;
 
 typedef struct {
@@ -579,7 +592,7 @@ static void refresh_window(const om_model* o, const om_rollout_args* a, om_img* 
     const int span = W < T - n_new ? W : T - n_new;
     for (int m = 1; m <= span; ++m) {
         const int pos = n_new + m;
-        const int i = pos - base - 1;
+        const int i = pos - base - 1 + ((g_debug & DBG_REUSE_SHIFT) ? 1 : 0);
         if (i >= 0 && i < nrows) {
             if (a->greedy) {
                 st->nz[m - 1] = om_argmax(st->guided + (size_t)i * V, V);
@@ -590,7 +603,8 @@ static void refresh_window(const om_model* o, const om_rollout_args* a, om_img* 
             }
             st->nmass[m - 1] = 0;
         } else {
-            const int src = pos - a->H >= 1 ? pos - a->H : pos - 1;
+            const int H = (g_debug & DBG_HISTORY_SHIFT) ? a->H - 1 : a->H;
+            const int src = pos - H >= 1 ? pos - H : pos - 1;
             st->nz[m - 1] = src <= n_new ? st->x[src] : st->nz[src - n_new - 1];
             st->nmass[m - 1] = 1;
         }
@@ -747,6 +761,25 @@ static void img_wasted_rows(const om_model* o, const om_rollout_args* a, om_img*
     free(rt);
 }
 
+static void record_window(const om_model* o, const om_rollout_args* a, const om_img* st,
+                          int* dr, float* q) {
+    const int W = a->W, T = o->T, V = o->m.V;
+    for (int b = 0; b < a->B; ++b) {
+        const om_img* s = &st[b];
+        const int span = s->n < T ? (W < T - s->n ? W : T - s->n) : 0;
+        for (int m = 0; m < W; ++m) {
+            int z = -1;
+            float qz = 0.0f;
+            if (m < span) {
+                z = s->wz[m];
+                qz = (a->greedy || s->wmass[m]) ? 1.0f : s->wq[(size_t)m * V + z];
+            }
+            dr[(size_t)b * W + m] = z;
+            q[(size_t)b * W + m] = qz;
+        }
+    }
+}
+
 int om_rollout(const om_model* o, const om_rollout_args* a, om_rollout_out* out) {
     const int B = a->B, T = o->T;
     if (a->W < 1 || a->H < 1 || B < 1) return -1;
@@ -754,6 +787,9 @@ int om_rollout(const om_model* o, const om_rollout_args* a, om_rollout_out* out)
     for (int b = 0; b < B; ++b) img_alloc(&st[b], o, a);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int b = 0; b < B; ++b) img_prefill(o, a, &st[b], b);
+    const size_t tw = (size_t)B * a->W;
+    if (out->trace_drafts && out->trace_q)
+        record_window(o, a, st, out->trace_drafts, out->trace_q);
     int rounds = 0, status = 0;
     for (;;) {
         int A = 0;
@@ -781,6 +817,8 @@ int om_rollout(const om_model* o, const om_rollout_args* a, om_rollout_out* out)
                 img_wasted_rows(o, a, &st[b], b);
         }
         ++rounds;
+        if (out->trace_drafts && out->trace_q)
+            record_window(o, a, st, out->trace_drafts + rounds * tw, out->trace_q + rounds * tw);
     }
     *out->rounds = rounds;
     long verified = 0, rejected = 0, imgrounds = 0;
