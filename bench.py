@@ -497,10 +497,9 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        from tests.gpu_util import bf16_rounded_blob
         cores = min(16, os.cpu_count() or 1)
         n_img = args.cpu_images or min(cores, B)
-        rb = bf16_rounded_blob(shape, blob) if wl.dtype == "bf16" else blob
+        rb = synth.bf16_rounded_blob(shape, blob) if wl.dtype == "bf16" else blob
         v, committed, dt = cpu_baseline(shape, rb, batch, wl, n_img, rounds=6)
         cpu = {"value": round(v, 2), "unit": "tokens/s", "cores": min(cores, n_img),
                "kind": "oracle",

@@ -196,11 +196,17 @@ hbsjd_status hbsjd_round(hbsjd_ctx* ctx, int32_t exec_mode, int32_t* counts, int
 /*
  * Export the rollout state to host arrays (any may be NULL): tokens [B][T]
  * (committed tokens, zero past the cursor), cursors [B] (committed count n_b),
- * drafts [B][W] (window position n_b + 1 + j; -1 past T) and draft_reused [B][W]
- * (1 if the draft is a reused prediction, 0 if a history token, -1 past T).
+ * drafts [B][W] (the draft at window position n_b + 1 + j; -1 past T and once
+ * the image is complete) and q_token_prob [B][W], the probability q(z) that
+ * each draft's proposal gives it (Sec. 4.2, Eq. 5): for a reused prediction
+ * (Sec. 4.2, "Independent rollout states") the p(z) of the verifier row it was
+ * drawn from; 1 for a history token (a point-mass proposal) and for every
+ * draft in greedy mode; 0 where drafts holds -1. The state is the one after
+ * hbsjd_rollout_begin (prefill and first window) or after the last
+ * hbsjd_round. ESTATE without a begin.
  */
 hbsjd_status hbsjd_get_state(hbsjd_ctx* ctx, int32_t* tokens, int32_t* cursors, int32_t* drafts,
-                             int32_t* draft_reused);
+                             float* q_token_prob);
 
 /*
  * Teacher-forced forward of n_seqs sequences [class, x_1..x_len] through the
@@ -251,15 +257,46 @@ hbsjd_status hbsjd_bikl_rows(const float* logits_s, const float* logits_t, int64
                              int32_t V, float* out, void* stream);
 
 /*
+ * The distribution transform of the verifier rows (Sec. 4.2: the target p and
+ * the reused proposals q are full-vocabulary distributions; guided logits under
+ * CFG, "Independent progress") on caller-supplied logits, with the draw each
+ * rollout row makes, for testing and for sampling outside a rollout. Per row r:
+ *   l = logits[r][0]                       (cfg = 1)
+ *   l = lu + cfg_scale (lc - lu)           (cfg = 2: lc = logits[r][0], lu = logits[r][1])
+ *   y = l / temperature[r]; with 0 < top_k < V, entries below the top_k-th
+ *   largest y (counting ties) are dropped, ties with it kept; p = softmax over
+ *   the kept entries, its normaliser summed sequentially inside 64-entry chunks
+ *   and then over the chunk totals.
+ * Outputs: p [rows][V]; argmax [rows], the first index of the largest l;
+ * draw [rows], the inverse-CDF draw from p (same association: the first entry
+ * whose chunk prefix plus in-chunk prefix exceeds u * sum p, else the last
+ * positive entry) with u = u_draft of Philox key `seed`, counter
+ * (r, position[r], 0, 0), position clamped to [0, 2^30].
+ * All pointers are device memory: logits fp32 [rows][cfg][V]; temperature fp32
+ * [rows] (finite and > 0; not checked); position int32 [rows]; p fp32
+ * [rows][V], which may be the logits buffer only when cfg = 1. Blocking.
+ * EINVAL before any device work for rows < 1, V not a multiple of 4 in
+ * [4, 16384], cfg not 1 or 2, a non-finite cfg_scale with cfg = 2, top_k < 0,
+ * a NULL buffer or p aliasing logits with cfg = 2; EINVAL after the transform
+ * when a logit is NaN (outputs then undefined); ENOMEM for its scratch (the
+ * per-row metadata, 8 bytes per row plus 64); EHIP.
+ */
+hbsjd_status hbsjd_transform_rows(int32_t rows, int32_t V, const float* logits, int32_t cfg,
+                                  float cfg_scale, const float* temperature, int32_t top_k,
+                                  uint64_t seed, const int32_t* position, float* p,
+                                  int32_t* argmax, int32_t* draw, void* stream);
+
+/*
  * The verification kernel (Sec. 4.2, Eq. 5) on caller-supplied rows, for
- * testing. All pointers are device memory: p and q fp32 [B][W][V] (target and
+ * testing; the acceptance test and the replacement draw are the rollout's own
+ * code. All pointers are device memory: p and q fp32 [B][W][V] (target and
  * proposal row of draft j), drafts [B][W], u_acc [B][W], u_res [B]. Draft j is
  * accepted iff p_j(z) >= q_j(z) or u_acc < p_j(z) / q_j(z); at the first
  * rejection the replacement is drawn with u_res from [p_j - q_j]_+ (from p_j when
- * that is all zero). Outputs: counts [B] (accepted drafts plus the replacement)
- * and tokens [B][W] (-1 past the count). V <= 16384. Drafts must lie in
- * [0, V); an image with a draft outside it gets count 0 and no tokens.
- * `stream` may be NULL.
+ * that is all zero in fp32). Outputs: counts [B] (accepted drafts plus the
+ * replacement) and tokens [B][W] (-1 past the count). V a multiple of 4 in
+ * [4, 16384] (EINVAL otherwise). Drafts must lie in [0, V); an image with a
+ * draft outside it gets count 0 and no tokens. `stream` may be NULL.
  */
 hbsjd_status hbsjd_verify_probs(int32_t B, int32_t W, int32_t V, const float* p, const float* q,
                                 const int32_t* drafts, const float* u_acc, const float* u_res,

@@ -65,6 +65,8 @@ _SIGS = {
     "hbsjd_score_bikl": (_I32, [_P, _P, _I32, _P, _P, _P, _P, _P]),
     "hbsjd_bikl_rows": (_I32, [_P, _P, ctypes.c_int64, _I32, _P, _P]),
     "hbsjd_verify_probs": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "hbsjd_transform_rows": (_I32, [_I32, _I32, _P, _I32, ctypes.c_float, _P, _I32,
+                                    ctypes.c_uint64, _P, _P, _P, _P, _P]),
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
     "hbsjd_profile_start": (_I32, [_P, ctypes.c_uint32]),
@@ -248,10 +250,10 @@ class Context:
         tokens = np.zeros((B, T), dtype=np.int32)
         cursors = np.zeros(B, dtype=np.int32)
         drafts = np.zeros((B, W), dtype=np.int32)
-        reused = np.zeros((B, W), dtype=np.int32)
+        q = np.zeros((B, W), dtype=np.float32)
         _check(self._lib.hbsjd_get_state(self._h, _np_ptr(tokens), _np_ptr(cursors),
-                                         _np_ptr(drafts), _np_ptr(reused)), "hbsjd_get_state")
-        return dict(tokens=tokens, cursors=cursors, drafts=drafts, reused=reused)
+                                         _np_ptr(drafts), _np_ptr(q)), "hbsjd_get_state")
+        return dict(tokens=tokens, cursors=cursors, drafts=drafts, q_token_prob=q)
 
     def hbsjd_forward(self, tokens, lens, labels):
         """Teacher-forced logits [sum(len+1), V] (fp32 device tensor)."""
@@ -314,6 +316,31 @@ def hbsjd_verify_probs(p, q, drafts, u_acc, u_res, stream=None):
                                 _P(_dev_ptr(tokens)), _P(_stream_handle(stream))),
            "hbsjd_verify_probs")
     return counts, tokens
+
+
+def hbsjd_transform_rows(logits, temperature, position, top_k: int = 0, cfg_scale: float = 0.0,
+                         seed: int = 0, stream=None, out=None):
+    """logits: fp32 device tensor [rows, V] or, with guidance, [rows, 2, V]
+    (conditional then unconditional row); temperature fp32 and position int32
+    device tensors [rows]. Returns (p [rows, V], argmax [rows], draw [rows])
+    device tensors, written into `out` when given."""
+    import torch
+    if logits.dim() == 2:
+        rows, V = logits.shape
+        cfg = 1
+    else:
+        rows, cfg, V = logits.shape
+    if out is None:
+        out = (torch.empty((rows, V), dtype=torch.float32, device=logits.device),
+               torch.empty(rows, dtype=torch.int32, device=logits.device),
+               torch.empty(rows, dtype=torch.int32, device=logits.device))
+    p, amax, draw = out
+    L = load_library()
+    _check(L.hbsjd_transform_rows(rows, V, _P(_dev_ptr(logits)), cfg, float(cfg_scale), _P(_dev_ptr(temperature)),
+              int(top_k), int(seed), _P(_dev_ptr(position)), _P(_dev_ptr(p)),
+              _P(_dev_ptr(amax)), _P(_dev_ptr(draw)), _P(_stream_handle(stream))),
+           "hbsjd_transform_rows")
+    return p, amax, draw
 
 
 def hbsjd_bikl_rows(logits_s, logits_t, stream=None):

@@ -75,12 +75,13 @@ struct hbsjd_ctx {
     DevBuf seg_seq, seg_row0, seg_nrows, seg_pos0;
     DevBuf slot_img, active_list, pf_slots;
     DevBuf h, hb, qb, ob, act, part;
-    DevBuf P[2], CP[2], amax[2], samp, logits;
+    DevBuf P[2], amax[2], samp, logits;
     DevBuf seq_row0, seq_img, seq_branch, lm_idx;
     DevBuf ptab, kv;
     DevBuf calib_tok;   // all-zero prefixes of the gamma calibration
     DevBuf seg_pages;   // [segment][max_pages] KV page of each tile (attention's page list)
     DevBuf win_end;     // [B] end of each image's current window (batch-synchronous progress)
+    DevBuf qz;          // [B][W] proposal probability of each draft (state export)
     DevBuf score_logits, score_idx, score_k;   // teacher scoring: selected logits rows, their
                                                // output slots, prefix lengths
     int32_t* pin = nullptr;    // pinned host words: active counts of the last two rounds
@@ -170,9 +171,9 @@ hbsjd_ctx::~hbsjd_ctx() {
                      &meta, &meta_pf, &a_hist, &mode_hist, &stats, &counts_own, &row_tok,
                      &row_pos, &row_kv, &row_seq, &seg_seq, &seg_row0, &seg_nrows, &seg_pos0,
                      &slot_img, &active_list, &pf_slots, &h, &hb, &qb, &ob, &act, &part, &P[0], &P[1],
-                     &CP[0], &CP[1], &amax[0], &amax[1], &samp, &logits, &seq_row0, &seq_img,
+                     &amax[0], &amax[1], &samp, &logits, &seq_row0, &seq_img,
                      &seq_branch, &lm_idx, &ptab, &kv, &calib_tok, &seg_pages, &win_end,
-                     &score_logits, &score_idx, &score_k};
+                     &score_logits, &score_idx, &score_k, &qz};
     for (DevBuf* b : all) free_buf(*b);
     if (pin) (void)hipHostFree(pin);
     for (auto& e : ev)
@@ -535,7 +536,6 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     TRY(ensure(c, c->lm_idx, std::max(n_seq, 1) * 4));
     for (int k = 0; k < 2; ++k) {
         TRY(ensure(c, c->P[k], (size_t)(cfg == 1 ? round_rows : out_rows) * c->V * 4));
-        TRY(ensure(c, c->CP[k], (size_t)out_rows * (c->nC + 1) * 4));
         TRY(ensure(c, c->amax[k], (size_t)out_rows * 4));
     }
     TRY(ensure(c, c->samp, (size_t)out_rows * 4));
@@ -636,13 +636,13 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
             c->m.rms_eps, c->d, c->hb.p, s);
     float* lg = cfg == 1 ? as<float>(c->P[1]) : as<float>(c->logits);
     gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, n_seq, lg, c->b_lm, s);
-    TransformArgs ta{lg, as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
+    TransformArgs ta{lg, as<float>(c->P[1]), as<int32_t>(c->amax[1]),
                      as<int32_t>(c->samp), as<int32_t>(c->pf_slots), as<int32_t>(c->cursor),
                      as<float>(c->temps), 1, cfg, c->V, c->top_k, T, c->cfg_scale,
                      mp + kMetaOutRows, (int)pslots.size(), as<int32_t>(c->meta)};
     transform(ta, s);
     VerifyArgs va{B, W, T, c->Hh, c->V, c->greedy, 1, 1, c->max_rounds,
-                  as<float>(c->P[1]), as<float>(c->CP[1]), as<int32_t>(c->amax[1]),
+                  as<float>(c->P[1]), as<int32_t>(c->amax[1]),
                   as<int32_t>(c->samp), nullptr, as<int32_t>(c->pf_slots), mp + kMetaImgs,
                   (int)pslots.size(),
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
@@ -685,7 +685,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
         gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg,
                     c->b_lm, s);
     }
-    TransformArgs ta{lg, as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
+    TransformArgs ta{lg, as<float>(c->P[cur]), as<int32_t>(c->amax[cur]),
                      as<int32_t>(c->samp), as<int32_t>(c->slot_img), as<int32_t>(c->cursor),
                      as<float>(c->temps), R, cfg, c->V, c->top_k, c->T, c->cfg_scale,
                      mt + kMetaOutRows, B * R, mt};
@@ -695,7 +695,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
     }
     if (!with_verify) return;
     VerifyArgs va{B, W, c->T, c->Hh, c->V, c->greedy, 0, R, c->max_rounds,
-                  as<float>(c->P[cur]), as<float>(c->CP[cur]), as<int32_t>(c->amax[cur]),
+                  as<float>(c->P[cur]), as<int32_t>(c->amax[cur]),
                   as<int32_t>(c->samp), as<float>(c->P[cur ^ 1]), as<int32_t>(c->slot_img),
                   mt + kMetaImgs, B,
                   as<int32_t>(c->cursor), as<int32_t>(c->xtok), as<int32_t>(c->drafts),
@@ -722,7 +722,7 @@ std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
                       &c->row_tok, &c->row_pos, &c->row_kv, &c->row_seq, &c->seg_seq,
                       &c->seg_row0, &c->seg_nrows, &c->seg_pos0, &c->slot_img,
                       &c->active_list, &c->h, &c->hb, &c->qb, &c->ob, &c->act, &c->part,
-                      &c->P[0], &c->P[1], &c->CP[0], &c->CP[1], &c->amax[0], &c->amax[1],
+                      &c->P[0], &c->P[1], &c->amax[0], &c->amax[1],
                       &c->samp, &c->logits, &c->ptab, &c->kv, &c->wbuf, &c->rope, &c->win_end,
                       &c->seg_pages};
     for (DevBuf* b : bufs) g.push_back((uint64_t)(uintptr_t)b->p);
@@ -1123,25 +1123,36 @@ hbsjd_status hbsjd_round(hbsjd_ctx* c, int32_t exec_mode, int32_t* counts, int32
 }
 
 hbsjd_status hbsjd_get_state(hbsjd_ctx* c, int32_t* tokens, int32_t* cursors, int32_t* drafts,
-                             int32_t* draft_reused) {
+                             float* q_token_prob) {
     try {
         GUARD(c);
         if (!c->have_state) return fail(HBSJD_ESTATE, "no rollout state");
         const int B = c->B, T = c->T, W = c->W;
-        std::vector<int32_t> x((size_t)B * T), n(B), dr((size_t)B * W), qs((size_t)B * W);
+        const size_t nw = (size_t)B * W;
+        std::vector<int32_t> x((size_t)B * T), n(B), dr(nw);
+        std::vector<float> qz(nw);
         hipStream_t s = c->stream;
+        if (q_token_prob && nw > 0) {
+            // the rows the window's reused drafts were drawn from: the prefill's
+            // buffer before any round, then the last round's
+            const int last = (c->rounds_launched + 1) & 1;
+            TRY(ensure(c, c->qz, nw * 4));
+            gather_q(as<float>(c->P[last]), as<int32_t>(c->qsrc), as<int32_t>(c->drafts), (int)nw,
+                     c->V, c->greedy, as<float>(c->qz), s);
+            HIPTRY(c, hipGetLastError());
+            HIPTRY(c, hipMemcpyAsync(qz.data(), c->qz.p, nw * 4, hipMemcpyDeviceToHost, s));
+        }
         HIPTRY(c, hipMemcpyAsync(x.data(), c->xtok.p, x.size() * 4, hipMemcpyDeviceToHost, s));
         HIPTRY(c, hipMemcpyAsync(n.data(), c->cursor.p, B * 4, hipMemcpyDeviceToHost, s));
-        HIPTRY(c, hipMemcpyAsync(dr.data(), c->drafts.p, dr.size() * 4, hipMemcpyDeviceToHost, s));
-        HIPTRY(c, hipMemcpyAsync(qs.data(), c->qsrc.p, qs.size() * 4, hipMemcpyDeviceToHost, s));
+        if (nw > 0)
+            HIPTRY(c, hipMemcpyAsync(dr.data(), c->drafts.p, nw * 4, hipMemcpyDeviceToHost, s));
         HIPTRY(c, hipStreamSynchronize(s));
         for (int b = 0; b < B; ++b)
             for (int t = n[b]; t < T; ++t) x[(size_t)b * T + t] = 0;
         if (tokens) std::memcpy(tokens, x.data(), x.size() * 4);
         if (cursors) std::memcpy(cursors, n.data(), B * 4);
-        if (drafts) std::memcpy(drafts, dr.data(), dr.size() * 4);
-        if (draft_reused)
-            for (size_t i = 0; i < qs.size(); ++i) draft_reused[i] = dr[i] < 0 ? -1 : (qs[i] >= 0 ? 1 : 0);
+        if (drafts && nw > 0) std::memcpy(drafts, dr.data(), nw * 4);
+        if (q_token_prob && nw > 0) std::memcpy(q_token_prob, qz.data(), nw * 4);
         return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_get_state");
@@ -1276,12 +1287,61 @@ hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
     }
 }
 
+namespace {
+hbsjd_status check_transform_rows(int32_t rows, int32_t V, const float* logits, int32_t cfg,
+                                  float cfg_scale, const float* temperature, int32_t top_k,
+                                  const int32_t* position, const float* p, const int32_t* argmax,
+                                  const int32_t* draw) {
+    if (rows < 1) return fail(HBSJD_EINVAL, "need rows >= 1");
+    if (V < 4 || V > kMaxVocab || V % 4) return fail(HBSJD_EINVAL, "need V a multiple of 4 in [4, 16384]");
+    if (cfg != 1 && cfg != 2) return fail(HBSJD_EINVAL, "cfg must be 1 or 2");
+    if (cfg == 2 && !std::isfinite(cfg_scale)) return fail(HBSJD_EINVAL, "cfg_scale not finite");
+    if (top_k < 0) return fail(HBSJD_EINVAL, "top_k < 0");
+    if (!logits || !temperature || !position || !p || !argmax || !draw)
+        return fail(HBSJD_EINVAL, "NULL buffer");
+    if (cfg == 2 && (const void*)p == (const void*)logits)
+        return fail(HBSJD_EINVAL, "p may alias logits only without guidance");
+    return HBSJD_OK;
+}
+
+hbsjd_status finish_transform_rows(const int32_t* meta, hipStream_t s) {
+    int32_t err = 0;
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) e = hipMemcpyAsync(&err, meta + kMetaError, 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("transform_rows: ") + hipGetErrorString(e));
+    if (err & kErrNanLogit) return fail(HBSJD_EINVAL, "a logit is NaN");
+    return HBSJD_OK;
+}
+}  // namespace
+
+hbsjd_status hbsjd_transform_rows(int32_t rows, int32_t V, const float* logits, int32_t cfg,
+                                  float cfg_scale, const float* temperature, int32_t top_k,
+                                  uint64_t seed, const int32_t* position, float* p,
+                                  int32_t* argmax, int32_t* draw, void* stream) {
+    try {
+        TRY(check_transform_rows(rows, V, logits, cfg, cfg_scale, temperature, top_k, position, p,
+                                 argmax, draw));
+        hipStream_t s = (hipStream_t)stream;
+        int32_t* scratch = nullptr;
+        hipError_t e = hipMalloc((void**)&scratch, transform_rows_scratch(rows) * 4);
+        if (e != hipSuccess) return fail(HBSJD_ENOMEM, "transform_rows scratch");
+        transform_rows(rows, V, logits, cfg, cfg_scale, temperature, top_k, seed, position, p,
+                       argmax, draw, scratch, s);
+        const hbsjd_status st = finish_transform_rows(scratch + 2 * (size_t)rows, s);
+        (void)hipFree(scratch);
+        return st;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_transform_rows");
+    }
+}
+
 hbsjd_status hbsjd_verify_probs(int32_t B, int32_t W, int32_t V, const float* p, const float* q,
                                 const int32_t* drafts, const float* u_acc, const float* u_res,
                                 int32_t* counts, int32_t* tokens, void* stream) {
     try {
-        if (B < 1 || W < 1 || V < 1 || V > kMaxVocab)
-            return fail(HBSJD_EINVAL, "need B >= 1, W >= 1, 1 <= V <= 16384");
+        if (B < 1 || W < 1 || V < 4 || V > kMaxVocab || V % 4)
+            return fail(HBSJD_EINVAL, "need B >= 1, W >= 1, V a multiple of 4 in [4, 16384]");
         if (!p || !q || !drafts || !u_acc || !u_res || !counts || !tokens)
             return fail(HBSJD_EINVAL, "NULL buffer");
         hipStream_t s = (hipStream_t)stream;

@@ -6,6 +6,8 @@
 
 #include <cstdint>
 
+#include "common.h"
+
 namespace hbsjd {
 
 // Optional kernel timing: when a caller arms the per-thread slot, the next
@@ -146,7 +148,6 @@ void philox_fill(uint64_t seed, int n, const uint32_t* bt, uint32_t* out, hipStr
 struct TransformArgs {
     const float* logits;     // forward rows [rows][V]
     float* p;                // distribution rows [out][V] (may equal logits without CFG)
-    float* cprefix;          // [out][nchunks + 1]
     int32_t* amax;           // [out]
     int32_t* samp;           // [out] each row's draw for the position it predicts (-1 past T)
     const int32_t* slot_img;
@@ -163,7 +164,6 @@ void transform(const TransformArgs& a, hipStream_t s);
 struct VerifyArgs {
     int B, W, T, H, V, greedy, prefill, rows_per_slot, max_rounds;   // seed comes from meta
     const float* p;          // this round's distribution rows
-    const float* cprefix;
     const int32_t* amax;
     const int32_t* samp;     // this round's draft candidates (from the transform)
     const float* p_prev;     // previous round's rows (proposals)
@@ -181,6 +181,19 @@ struct VerifyArgs {
     const int32_t* win_end = nullptr;   // batch-synchronous windows: verify up to win_end[b]
 };
 void verify_commit(const VerifyArgs& a, hipStream_t s);
+// q[i] for the state export: p(z) of a reused draft's source row, 1 for a
+// history draft or in greedy mode, 0 without a draft
+void gather_q(const float* P, const int32_t* qsrc, const int32_t* drafts, int n, int V,
+              int greedy, float* q, hipStream_t s);
+
+// The transform of caller rows (row r = image r at position pos[r], clamped to
+// [0, kRowPosMax]): logits [rows][cfg][V]; outputs p [rows][V], amax and draw
+// [rows]. `scratch` holds transform_rows_scratch(rows) int32 words.
+constexpr int kRowPosMax = 1 << 30;
+inline size_t transform_rows_scratch(int rows) { return 2 * (size_t)rows + kMetaCount; }
+void transform_rows(int rows, int V, const float* logits, int cfg, float cfg_scale,
+                    const float* temperature, int top_k, uint64_t seed, const int32_t* pos,
+                    float* p, int32_t* amax, int32_t* draw, int32_t* scratch, hipStream_t s);
 
 // ---------------------------------------------------------------- teacher scoring
 // per row r: D_biKL(softmax(ls[r]), softmax(lt[r])) into out[out_idx ? out_idx[r] : r]

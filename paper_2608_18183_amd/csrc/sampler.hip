@@ -377,13 +377,12 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
         }
     }
     __syncthreads();
-    float* cp = a.cprefix + (size_t)r * (nC + 1);
-    for (int c = t; c <= nC; c += 256) cp[c] = tot[c];
 
     // draft candidate of this row: the position it predicts is n_b + i + 1 no
     // matter how the round's verification ends, so its draw from p with
-    // u_draft(b, n_b + i + 1) is taken here, with the row's own prefix; the
-    // same search as wave_sample_cp, hence the same token
+    // u_draft(b, n_b + i + 1) is taken here, with the row's own prefix: the
+    // same sums and search as block_inv_cdf_regs over the stored row, hence
+    // the same token
     int z_draft = -1;
     if (pos <= a.T) {
         const float target = u_draft * tot[nC];
@@ -399,8 +398,7 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
         if (cs == 0x7fffffff) {   // rounding left the target above the total
             z_draft = s_int[2];
         } else {
-            // the owner parks its chunk; wavefront 0 scans it in order, lane k
-            // holding entry k (the same sums as wave_sample_cp)
+            // the owner parks its chunk in LDS and thread 0 scans it in order
             if (t == cs) {
 #pragma unroll
                 for (int k = 0; k < kChunk; k += 4)
@@ -444,99 +442,11 @@ void transform(const TransformArgs& a, hipStream_t s) {
 
 // ---------------------------------------------------------------- inverse CDF helpers
 
-// Wave-level draw from a distribution row with its chunk prefix cp[0..nC].
-__device__ inline int wave_sample_cp(const float* prow, const float* cp, int V, int nC, float u) {
-    const int lane = threadIdx.x & 63;
-    const float target = u * cp[nC];
-    int cs = 0x7fffffff;
-    for (int c = lane; c < nC; c += 64)
-        if (cp[c + 1] > target) { cs = c; break; }
-    cs = wave_min_int(cs);
-    if (cs == 0x7fffffff) {
-        int last = -1;
-        for (int v = lane; v < V; v += 64)
-            if (prow[v] > 0.f) last = v;
-        return wave_max_int(last);
-    }
-    const int v = cs * kChunk + lane;
-    const float pv = v < V ? prow[v] : 0.f;
-    const float before = cp[cs];
-    float inner = 0.f;
-    int found = -1, lastpos = -1;
-    for (int k = 0; k < kChunk; ++k) {
-        const float x = __shfl(pv, k, 64);
-        if (cs * kChunk + k >= V) break;
-        inner = inner + x;
-        if (x > 0.f) lastpos = cs * kChunk + k;
-        if (before + inner > target) { found = cs * kChunk + k; break; }
-    }
-    return found >= 0 ? found : lastpos;
-}
-
-// Block-level draw from non-negative weights w(v) computed on the fly; returns
-// -1 when every weight is zero. All 256 threads must call it.
-template <typename F>
-__device__ int block_inv_cdf(F w, int V, float u, float* cp, int* res) {
-    const int t = threadIdx.x;
-    const int nC = (V + kChunk - 1) / kChunk;
-    for (int c = t; c < nC; c += 256) {
-        float sum = 0.f;
-        for (int k = 0; k < kChunk; ++k) {
-            const int v = c * kChunk + k;
-            if (v < V) sum = sum + w(v);
-        }
-        cp[c + 1] = sum;
-    }
-    __syncthreads();
-    if (t == 0) {
-        float run = 0.f;
-        cp[0] = 0.f;
-        for (int c = 0; c < nC; ++c) {
-            run = run + cp[c + 1];
-            cp[c + 1] = run;
-        }
-    }
-    __syncthreads();
-    const float total = cp[nC];
-    if (!(total > 0.f)) return -1;
-    if (t < 64) {
-        const int lane = t;
-        const float target = u * total;
-        int cs = 0x7fffffff;
-        for (int c = lane; c < nC; c += 64)
-            if (cp[c + 1] > target) { cs = c; break; }
-        cs = wave_min_int(cs);
-        int out;
-        if (cs == 0x7fffffff) {
-            int last = -1;
-            for (int v = lane; v < V; v += 64)
-                if (w(v) > 0.f) last = v;
-            out = wave_max_int(last);
-        } else {
-            const int v = cs * kChunk + lane;
-            const float pv = v < V ? w(v) : 0.f;
-            const float before = cp[cs];
-            float inner = 0.f;
-            int found = -1, lastpos = -1;
-            for (int k = 0; k < kChunk; ++k) {
-                const float x = __shfl(pv, k, 64);
-                if (cs * kChunk + k >= V) break;
-                inner = inner + x;
-                if (x > 0.f) lastpos = cs * kChunk + k;
-                if (before + inner > target) { found = cs * kChunk + k; break; }
-            }
-            out = found >= 0 ? found : lastpos;
-        }
-        if (lane == 0) *res = out;
-    }
-    __syncthreads();
-    return *res;
-}
-
-// Block-level draw from non-negative weights held chunk-owned in registers
-// (thread t has entries 64 t .. 64 t + 63 in w); the same association and the
-// same answer as block_inv_cdf. Returns -1 when every weight is zero. All 256
-// threads must call it.
+// Block-level inverse CDF over non-negative weights held chunk-owned in
+// registers (thread t has entries 64 t .. 64 t + 63 in w), in the pinned
+// association: the first entry whose chunk prefix plus in-chunk prefix exceeds
+// u * total, else the last positive entry. Returns -1 when every weight is
+// zero. All 256 threads must call it.
 __device__ inline int block_inv_cdf_regs(const float (&w)[kChunk], int V, float u, float* cp,
                                          int* res) {
     const int t = threadIdx.x;
@@ -597,6 +507,35 @@ __device__ inline int block_inv_cdf_regs(const float (&w)[kChunk], int V, float 
     return *res;
 }
 
+// The replacement token of a rejected draft (Sec. 4.2, Eq. 5): a draw with u
+// from the residual max(0, p - q), where q is the proposal row `qrow`, or a
+// point mass on z when qrow is null (a history draft); from p itself when the
+// residual is zero everywhere in fp32. All 256 threads must call it.
+__device__ int replacement_draw(const float* __restrict__ pr, const float* __restrict__ qrow,
+                                int z, int V, float u, float* stage, float* cp, int* res) {
+    const int t = threadIdx.x;
+    float w[kChunk];
+    stage_load_row(pr, V, stage, [&](int k, float x) { w[k] = x; });
+    if (qrow) {
+        stage_load_row(qrow, V, stage, [&](int k, float x) {
+            const float d = w[k] - x;
+            w[k] = d > 0.f ? d : 0.f;
+        });
+    } else {
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) {
+            const float d = w[k] - (t * kChunk + k == z ? 1.0f : 0.0f);
+            w[k] = d > 0.f ? d : 0.f;
+        }
+    }
+    int rep = block_inv_cdf_regs(w, V, u, cp, res);
+    if (rep < 0) {   // the residual underflowed: draw from p
+        stage_load_row(pr, V, stage, [&](int k, float x) { w[k] = x; });
+        rep = block_inv_cdf_regs(w, V, u, cp, res);
+    }
+    return rep;
+}
+
 // ---------------------------------------------------------------- verify + commit + refresh
 // One 256-thread block per processed image.
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
@@ -614,7 +553,6 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     const int n = a.cursor[b];
     if (n >= a.T) return;              // finished image in Full mode: rows discarded
     const int W = a.W, V = a.V, R = a.rows_per_slot;
-    const int nC = (V + kChunk - 1) / kChunk;
     const uint64_t seed = meta_seed(a.meta);
     if (a.ar) {
         // cached AR: the image's single row predicts position n + 1 (Eq. 1)
@@ -673,34 +611,11 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
             if (a.greedy) {
                 rep = a.amax[prow];
             } else {
-                const float* pr = a.p + (size_t)prow * V;
                 const int qs = old_q[js - 1];
-                const int z = old_dr[js - 1];
                 const float u = uniforms_at(seed, b, n + js).res;
-                // residual max(0, p - q) of the rejected position, chunk-owned
-                float w[kChunk];
-                stage_load_row(pr, V, stage, [&](int k, float x) { w[k] = x; });
-                if (qs >= 0) {
-                    stage_load_row(a.p_prev + (size_t)qs * V, V, stage, [&](int k, float x) {
-                        const float d = w[k] - x;
-                        w[k] = d > 0.f ? d : 0.f;
-                    });
-                } else {   // history draft: point-mass proposal on z
-#pragma unroll
-                    for (int k = 0; k < kChunk; ++k) {
-                        const float d = w[k] - (t * kChunk + k == z ? 1.0f : 0.0f);
-                        w[k] = d > 0.f ? d : 0.f;
-                    }
-                }
-                rep = block_inv_cdf_regs(w, V, u, cp, &s_res);
-                if (rep < 0) {
-                    if (t < 64) {
-                        const int got = wave_sample_cp(pr, a.cprefix + (size_t)prow * (nC + 1), V, nC, u);
-                        if (t == 0) s_res = got;
-                    }
-                    __syncthreads();
-                    rep = s_res;
-                }
+                rep = replacement_draw(a.p + (size_t)prow * V,
+                                       qs >= 0 ? a.p_prev + (size_t)qs * V : nullptr,
+                                       old_dr[js - 1], V, u, stage, cp, &s_res);
             }
         }
         // commit x_{n+1..n+count}
@@ -764,12 +679,69 @@ void verify_commit(const VerifyArgs& a, hipStream_t s) {
     launch(k_verify, dim3(a.nimg_cap), dim3(256), 0, s, a);
 }
 
+// ---------------------------------------------------------------- state export
+// q[i] = the proposal probability of draft i: its source row's p(z) for a
+// reused prediction (qsrc >= 0) in probabilistic mode, 1 for a history draft
+// (point mass) or in greedy mode, 0 where there is no draft
+__global__ void k_gather_q(const float* __restrict__ P, const int32_t* __restrict__ qsrc,
+                           const int32_t* __restrict__ drafts, int n, int V, int greedy,
+                           float* __restrict__ q) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int z = drafts[i], qs = qsrc[i];
+    float v = 0.f;
+    if (z >= 0) v = (greedy || qs < 0) ? 1.0f : P[(size_t)qs * V + z];
+    q[i] = v;
+}
+
+void gather_q(const float* P, const int32_t* qsrc, const int32_t* drafts, int n, int V,
+              int greedy, float* q, hipStream_t s) {
+    if (n <= 0) return;
+    launch(k_gather_q, dim3((n + 255) / 256), dim3(256), 0, s, P, qsrc, drafts, n, V, greedy, q);
+}
+
+// ---------------------------------------------------------------- explicit-row transform
+// Metadata of a transform over caller rows: row r is image r at sequence
+// position pos[r] (clamped to [0, kRowPosMax]); the row's draw then uses
+// u_draft(seed, r, pos[r]).
+__global__ void k_transform_rows_setup(int rows, uint32_t seed_lo, uint32_t seed_hi,
+                                       const int32_t* __restrict__ pos, int32_t* slot_img,
+                                       int32_t* cursor, int32_t* meta) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < rows) {
+        slot_img[i] = i;
+        cursor[i] = min(max(pos[i], 0), kRowPosMax) - 1;
+    }
+    if (i < kMetaCount) {
+        int v = 0;
+        if (i == kMetaOutRows) v = rows;
+        if (i == kMetaSeedLo) v = (int32_t)seed_lo;
+        if (i == kMetaSeedHi) v = (int32_t)seed_hi;
+        meta[i] = v;
+    }
+}
+
+void transform_rows(int rows, int V, const float* logits, int cfg, float cfg_scale,
+                    const float* temperature, int top_k, uint64_t seed, const int32_t* pos,
+                    float* p, int32_t* amax, int32_t* draw, int32_t* scratch, hipStream_t s) {
+    int32_t* slot_img = scratch;
+    int32_t* cursor = scratch + rows;
+    int32_t* meta = scratch + 2 * (size_t)rows;
+    const int n = rows > kMetaCount ? rows : kMetaCount;
+    launch(k_transform_rows_setup, dim3((n + 255) / 256), dim3(256), 0, s, rows, (uint32_t)seed,
+           (uint32_t)(seed >> 32), pos, slot_img, cursor, meta);
+    TransformArgs a{logits, p, amax, draw, slot_img, cursor, temperature, 1, cfg, V, top_k,
+                    kRowPosMax, cfg_scale, meta + kMetaOutRows, rows, meta};
+    transform(a, s);
+}
+
 // ---------------------------------------------------------------- explicit-row verification
 __global__ __launch_bounds__(256) void k_verify_probs(int W, int V, const float* p, const float* q,
                                                       const int32_t* drafts, const float* u_acc,
                                                       const float* u_res, int32_t* counts,
                                                       int32_t* tokens) {
     __shared__ float cp[kMaxChunks + 1];
+    __shared__ __attribute__((aligned(16))) float stage[kStageFloats];
     __shared__ int s_res, s_first;
     __shared__ int s_bad;
     const int b = blockIdx.x, t = threadIdx.x;
@@ -802,16 +774,9 @@ __global__ __launch_bounds__(256) void k_verify_probs(int W, int V, const float*
     const int count = rejected ? js : W;
     int rep = 0;
     if (rejected) {
-        const float* pr = p + ((size_t)b * W + js - 1) * V;
-        const float* qr = q + ((size_t)b * W + js - 1) * V;
-        const float u = u_res[b];
-        rep = block_inv_cdf(
-            [=](int v) {
-                const float d = pr[v] - qr[v];
-                return d > 0.f ? d : 0.f;
-            },
-            V, u, cp, &s_res);
-        if (rep < 0) rep = block_inv_cdf([=](int v) { return pr[v]; }, V, u, cp, &s_res);
+        const size_t row = (size_t)b * W + js - 1;
+        rep = replacement_draw(p + row * V, q + row * V, drafts[row], V, u_res[b], stage, cp,
+                               &s_res);
     }
     for (int j = t; j < W; j += 256) {
         const size_t row = (size_t)b * W + j;

@@ -144,6 +144,24 @@ def make_weights(m: ModelShape, seed: int = 0, std: float = 0.02,
     return blob
 
 
+def bf16_rounded_blob(m: ModelShape, blob: np.ndarray) -> np.ndarray:
+    """The weights a bf16 workload uses: every matrix and embedding of the blob
+    rounded to the nearest bf16 (ties to even) and returned as fp32; RMSNorm
+    gains and the lm_head bias stay fp32. Both the GPU (which rounds the blob
+    it is given the same way) and the fp32 oracle of a bf16 comparison see
+    these values."""
+    out = np.array(blob, dtype=np.float32, copy=True)
+    off = 0
+    for _, shape, kind in blob_layout(m):
+        k = int(np.prod(shape))
+        if kind == "w":
+            u = out[off:off + k].view(np.uint32)
+            u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+            u &= np.uint32(0xFFFF0000)
+        off += k
+    return out
+
+
 def split_blob(m: ModelShape, blob: np.ndarray) -> Dict[str, np.ndarray]:
     """Named views into a blob (no copies)."""
     out, off = {}, 0

@@ -24,16 +24,8 @@ def make_ctx(shape, dtype, blob, max_kv_bytes=0):
 
 
 def bf16_rounded_blob(shape, blob):
-    """The blob as a bf16 context holds it: matrices and embeddings rounded to
-    bf16 (nearest-even), gains and the lm_head bias left in fp32."""
-    out = blob.copy()
-    off = 0
-    for _, shp, kind in synth.blob_layout(shape):
-        k = int(np.prod(shp))
-        if kind == "w":
-            out[off:off + k] = oracle.round_bf16(blob[off:off + k])
-        off += k
-    return out
+    """The blob as a bf16 context holds it (see synth.bf16_rounded_blob)."""
+    return synth.bf16_rounded_blob(shape, blob)
 
 
 def device_batch(batch):
