@@ -49,7 +49,12 @@ typedef enum hbsjd_status {
 
 typedef enum hbsjd_dtype {
     HBSJD_DTYPE_F32 = 0,  /* fp32 weights, activations and KV cache */
-    HBSJD_DTYPE_BF16 = 1  /* bf16 weights and KV cache, fp32 accumulation and sampling */
+    /* bf16 weights (rounded to nearest-even on load), held on the GPU as fp16
+     * times a power-of-two scale per matrix, exact for every weight down to
+     * 2^-31 of its matrix's largest magnitude; fp16 MFMA operands, activations
+     * and KV cache (the bf16 operand width and rate, three more mantissa bits);
+     * fp32 embeddings, residual stream, accumulation and sampling */
+    HBSJD_DTYPE_BF16 = 1
 } hbsjd_dtype;
 
 typedef enum hbsjd_exec_mode {

@@ -49,7 +49,7 @@ struct DevBuf {
 struct hbsjd_ctx {
     hbsjd_model_desc m{};
     int L = 0, d = 0, H = 0, dh = 0, f = 0, V = 0, C = 0, G = 0, T = 0, nC = 0;
-    bool bf16 = false;
+    bool f16 = false;
     size_t esz = 4;
     hipStream_t stream = nullptr;       // the library's own stream (default priority)
     hipStream_t user_stream = nullptr;  // the caller's stream: work starts after its work
@@ -62,8 +62,12 @@ struct hbsjd_ctx {
 
     // weights
     DevBuf wbuf;
-    void *tok_emb = nullptr, *cls_emb = nullptr, *w_lm = nullptr;
+    float *tok_emb = nullptr, *cls_emb = nullptr;
+    void* w_lm = nullptr;
     float *b_lm = nullptr, *g_out = nullptr;
+    // per GEMM matrix: the factor that undoes its storage scale (1 for fp32)
+    std::vector<float> s_qkv, s_o, s_13, s_2;
+    float s_lm = 1.f;
     std::vector<float*> g_attn, g_ffn;
     std::vector<void*> wqkv, wo, w13, w2;
     DevBuf rope;   // cos then sin, [(T+1)][dh/2] each
@@ -263,10 +267,10 @@ std::string check_model(const hbsjd_model_desc& m) {
     if (m.vocab % 4) return "vocab must be a multiple of 4";
     if (m.dtype != HBSJD_DTYPE_F32 && m.dtype != HBSJD_DTYPE_BF16) return "unknown dtype";
     if (m.dtype == HBSJD_DTYPE_BF16) {
-        if (dh != 64) return "bf16 needs head_dim 64";
-        if (m.d_model % 64) return "bf16 needs d_model a multiple of 64";
-        if (m.mlp_hidden % 64) return "bf16 needs mlp_hidden a multiple of 64";
-        if (m.vocab % 64) return "bf16 needs vocab a multiple of 64";
+        if (dh != 64) return "a bf16 model needs head_dim 64";
+        if (m.d_model % 64) return "a bf16 model needs d_model a multiple of 64";
+        if (m.mlp_hidden % 64) return "a bf16 model needs mlp_hidden a multiple of 64";
+        if (m.vocab % 64) return "a bf16 model needs vocab a multiple of 64";
     } else {
         if (dh > 64) return "fp32 needs head_dim <= 64";
         if ((long)m.grid * m.grid > 959) return "fp32 needs grid^2 <= 959";
@@ -303,7 +307,7 @@ void* kv_layer(hbsjd_ctx* c, int l) {
 // decoder layers; leaves the residual stream in h and its final RMSNorm (gain
 // g_out) in hb
 void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
-    const bool bf = c->bf16;
+    const bool bf = c->f16;
     hipStream_t s = c->stream;
     const int d = c->d, f = c->f;
     {
@@ -317,7 +321,8 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         QkvArgs qa{c->qb.p, kv_layer(c, l), r.meta.pos, r.meta.kv, rc, rs, d, c->H, c->dh, c->T};
         {
             Timed tm(c, HBSJD_K_QKV);
-            gemm_qkv(bf, c->hb.p, d, c->wqkv[l], 3 * d, d, r.nrows_dev, r.nrows_cap, qa, s);
+            gemm_qkv(bf, c->hb.p, d, c->wqkv[l], c->s_qkv[l], 3 * d, d, r.nrows_dev, r.nrows_cap,
+                     qa, s);
         }
         {
             Timed tm(c, HBSJD_K_ATTN);
@@ -330,8 +335,8 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         const int s2 = bf ? split_for(r.nrows_cap, d, f) : 1;
         {
             Timed tm(c, HBSJD_K_OPROJ);
-            gemm_partial(bf, 0, c->ob.p, d, c->wo[l], d, d, r.nrows_dev, r.nrows_cap, so,
-                         as<float>(c->part), s);
+            gemm_partial(bf, 0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev, r.nrows_cap,
+                         so, as<float>(c->part), s);
         }
         {
             Timed tm(c, HBSJD_K_NORM);
@@ -340,12 +345,13 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         }
         {
             Timed tm(c, HBSJD_K_W13);
-            gemm_swiglu(bf, c->hb.p, d, c->w13[l], 2 * f, d, r.nrows_dev, r.nrows_cap, c->act.p, s);
+            gemm_swiglu(bf, c->hb.p, d, c->w13[l], c->s_13[l], 2 * f, d, r.nrows_dev, r.nrows_cap,
+                        c->act.p, s);
         }
         {
             Timed tm(c, HBSJD_K_W2);
-            gemm_partial(bf, 1, c->act.p, f, c->w2[l], d, f, r.nrows_dev, r.nrows_cap, s2,
-                         as<float>(c->part), s);
+            gemm_partial(bf, 1, c->act.p, f, c->w2[l], c->s_2[l], d, f, r.nrows_dev, r.nrows_cap,
+                         s2, as<float>(c->part), s);
         }
         {
             // the next layer's attention norm, or the final norm after the last layer
@@ -372,7 +378,7 @@ hbsjd_status ensure_acts(hbsjd_ctx* c, long rows) {
     TRY(ensure(c, c->row_pos, rows * 4));
     TRY(ensure(c, c->row_kv, rows * 4));
     TRY(ensure(c, c->row_seq, rows * 4));
-    const long sp = c->bf16 ? std::max(split_for((int)rows, c->d, c->d),
+    const long sp = c->f16 ? std::max(split_for((int)rows, c->d, c->d),
                                        split_for((int)rows, c->d, c->f))
                             : 1;
     TRY(ensure(c, c->part, (size_t)sp * rows * d * 4));
@@ -441,7 +447,7 @@ hbsjd_status validate_args(const hbsjd_ctx* c, const hbsjd_rollout_args* a) {
         return fail(HBSJD_EINVAL, "unknown progress mode");
     if (!a->prefix_tokens || !a->prefix_len || !a->class_labels || !a->temperature)
         return fail(HBSJD_EINVAL, "prefix_tokens, prefix_len, class_labels and temperature are required");
-    if (!c->bf16 && c->T + (ar ? 0 : a->window) + 1 > 1024)
+    if (!c->f16 && c->T + (ar ? 0 : a->window) + 1 > 1024)
         return fail(HBSJD_EINVAL, "fp32 mode supports T + window + 1 <= 1024");
     int need = 0;
     for (int b = 0; b < a->batch; ++b) {
@@ -632,10 +638,10 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
         return HBSJD_OK;
     }
     // final norm of each sequence's last row, lm_head, transform, first window
-    rmsnorm(c->bf16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, n_seq, c->g_out,
+    rmsnorm(c->f16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, n_seq, c->g_out,
             c->m.rms_eps, c->d, c->hb.p, s);
     float* lg = cfg == 1 ? as<float>(c->P[1]) : as<float>(c->logits);
-    gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, n_seq, lg, c->b_lm, s);
+    gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d, mp + kMetaActive, n_seq, lg, c->b_lm, s);
     TransformArgs ta{lg, as<float>(c->P[1]), as<int32_t>(c->amax[1]),
                      as<int32_t>(c->samp), as<int32_t>(c->pf_slots), as<int32_t>(c->cursor),
                      as<float>(c->temps), 1, cfg, c->V, c->top_k, T, c->cfg_scale,
@@ -682,7 +688,7 @@ void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
     float* lg = cfg == 1 ? as<float>(c->P[cur]) : as<float>(c->logits);
     {
         Timed tm(c, HBSJD_K_LMHEAD);
-        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg,
+        gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d, mt + kMetaRows, rows_cap, lg,
                     c->b_lm, s);
     }
     TransformArgs ta{lg, as<float>(c->P[cur]), as<int32_t>(c->amax[cur]),
@@ -876,8 +882,8 @@ hbsjd_status hbsjd_create(const hbsjd_model_desc* m, uint64_t max_kv_bytes, void
         c->G = m->grid;
         c->T = m->grid * m->grid;
         c->nC = (c->V + kChunk - 1) / kChunk;
-        c->bf16 = m->dtype == HBSJD_DTYPE_BF16;
-        c->esz = c->bf16 ? 2 : 4;
+        c->f16 = m->dtype == HBSJD_DTYPE_BF16;
+        c->esz = c->f16 ? 2 : 4;
         c->user_stream = (hipStream_t)stream;
         c->max_kv_bytes = max_kv_bytes;
         hipError_t e = hipGetDevice(&c->device);
@@ -936,16 +942,18 @@ hbsjd_status hbsjd_load_weights(hbsjd_ctx* c, const float* blob, size_t n_floats
             return fail(HBSJD_EINVAL, "blob has " + std::to_string(n_floats) + " floats, model needs " +
                                           std::to_string(blob_floats(c)));
         const size_t d = c->d, f = c->f, V = c->V, C = c->C, L = c->L, es = c->esz;
-        // device layout: matrices in the compute dtype, gains and bias fp32,
-        // W1|W3 interleaved by rows (row 2i = W1 row i, row 2i+1 = W3 row i)
+        // device layout: embeddings, gains and bias fp32; the GEMM matrices in
+        // the compute type (for a bf16 model: rounded to bf16, then held as fp16
+        // times a power-of-two scale, see common.h), W1|W3 interleaved by rows
+        // (row 2i = W1 row i, row 2i+1 = W3 row i)
         std::vector<size_t> off;
         size_t total = 0;
         auto take = [&](size_t bytes) {
             off.push_back(total);
             total += (bytes + 255) & ~(size_t)255;
         };
-        take(V * d * es);            // tok_emb
-        take((C + 1) * d * es);      // cls_emb
+        take(V * d * 4);             // tok_emb
+        take((C + 1) * d * 4);       // cls_emb
         for (size_t l = 0; l < L; ++l) {
             take(d * 4);             // g_attn
             take(3 * d * d * es);    // wqkv
@@ -958,23 +966,42 @@ hbsjd_status hbsjd_load_weights(hbsjd_ctx* c, const float* blob, size_t n_floats
         take(V * d * es);            // w_lm
         if (c->m.has_lm_bias) take(V * 4);
         std::vector<unsigned char> host(total, 0);
-        auto put = [&](size_t dst, const float* src, size_t n, bool mat) {
-            if (mat && c->bf16) {
-                uint16_t* o = reinterpret_cast<uint16_t*>(host.data() + dst);
-                for (size_t i = 0; i < n; ++i) o[i] = f32_to_bf16(src[i]);
-            } else {
-                std::memcpy(host.data() + dst, src, n * 4);
-            }
+        // fp32 values (embeddings of a bf16 model rounded to bf16)
+        auto put_f32 = [&](size_t dst, const float* src, size_t n, bool round) {
+            float* o = reinterpret_cast<float*>(host.data() + dst);
+            for (size_t i = 0; i < n; ++i) o[i] = round ? bf16_to_f32(f32_to_bf16(src[i])) : src[i];
         };
+        // a GEMM matrix; returns the factor its sums are multiplied by
+        auto put_mat = [&](size_t dst, const float* src, size_t n) -> float {
+            if (!c->f16) {
+                std::memcpy(host.data() + dst, src, n * 4);
+                return 1.0f;
+            }
+            float mx = 0.f;
+            for (size_t i = 0; i < n; ++i) mx = std::max(mx, std::fabs(bf16_to_f32(f32_to_bf16(src[i]))));
+            // scale 2^e with the largest magnitude in [2^14, 2^15)
+            int e = 0;
+            if (mx > 0.f) {
+                int ex = 0;
+                std::frexp(mx, &ex);   // mx in [2^(ex-1), 2^ex)
+                e = 15 - ex;
+            }
+            const float sc = std::ldexp(1.0f, e);
+            uint16_t* o = reinterpret_cast<uint16_t*>(host.data() + dst);
+            for (size_t i = 0; i < n; ++i) o[i] = f32_to_f16_bits_host(bf16_to_f32(f32_to_bf16(src[i])) * sc);
+            return std::ldexp(1.0f, -e);
+        };
+        const bool rnd = c->f16;
         const float* p = blob;
         size_t k = 0;
-        put(off[k++], p, V * d, true); p += V * d;
-        put(off[k++], p, (C + 1) * d, true); p += (C + 1) * d;
+        put_f32(off[k++], p, V * d, rnd); p += V * d;
+        put_f32(off[k++], p, (C + 1) * d, rnd); p += (C + 1) * d;
+        c->s_qkv.assign(L, 1.f); c->s_o.assign(L, 1.f); c->s_13.assign(L, 1.f); c->s_2.assign(L, 1.f);
         for (size_t l = 0; l < L; ++l) {
-            put(off[k++], p, d, false); p += d;
-            put(off[k++], p, 3 * d * d, true); p += 3 * d * d;
-            put(off[k++], p, d * d, true); p += d * d;
-            put(off[k++], p, d, false); p += d;
+            put_f32(off[k++], p, d, false); p += d;
+            c->s_qkv[l] = put_mat(off[k++], p, 3 * d * d); p += 3 * d * d;
+            c->s_o[l] = put_mat(off[k++], p, d * d); p += d * d;
+            put_f32(off[k++], p, d, false); p += d;
             {
                 const float* w1 = p;
                 const float* w3 = p + f * d;
@@ -983,20 +1010,20 @@ hbsjd_status hbsjd_load_weights(hbsjd_ctx* c, const float* blob, size_t n_floats
                     std::memcpy(&il[(2 * i) * d], w1 + i * d, d * 4);
                     std::memcpy(&il[(2 * i + 1) * d], w3 + i * d, d * 4);
                 }
-                put(off[k++], il.data(), 2 * f * d, true);
+                c->s_13[l] = put_mat(off[k++], il.data(), 2 * f * d);
                 p += 2 * f * d;
             }
-            put(off[k++], p, d * f, true); p += d * f;
+            c->s_2[l] = put_mat(off[k++], p, d * f); p += d * f;
         }
-        put(off[k++], p, d, false); p += d;
-        put(off[k++], p, V * d, true); p += V * d;
-        if (c->m.has_lm_bias) { put(off[k++], p, V, false); p += V; }
+        put_f32(off[k++], p, d, false); p += d;
+        c->s_lm = put_mat(off[k++], p, V * d); p += V * d;
+        if (c->m.has_lm_bias) { put_f32(off[k++], p, V, false); p += V; }
         TRY(ensure(c, c->wbuf, total));
         HIPTRY(c, hipMemcpy(c->wbuf.p, host.data(), total, hipMemcpyHostToDevice));
         char* base = (char*)c->wbuf.p;
         k = 0;
-        c->tok_emb = base + off[k++];
-        c->cls_emb = base + off[k++];
+        c->tok_emb = (float*)(base + off[k++]);
+        c->cls_emb = (float*)(base + off[k++]);
         c->g_attn.assign(L, nullptr); c->g_ffn.assign(L, nullptr);
         c->wqkv.assign(L, nullptr); c->wo.assign(L, nullptr);
         c->w13.assign(L, nullptr); c->w2.assign(L, nullptr);
@@ -1176,7 +1203,7 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         }
         TRY(forward_core(c, n_seqs, tokens, lab, ln, simg, ln, row0));
         const int rows = row0.back();
-        gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d,
+        gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d,
                     as<int32_t>(c->meta_pf) + kMetaRows, rows, logits, c->b_lm, c->stream);
         HIPTRY(c, hipGetLastError());
         HIPTRY(c, hipStreamSynchronize(c->stream));
@@ -1254,9 +1281,9 @@ hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
                                          hipMemcpyHostToDevice, c->stream));
                 int32_t* mp = as<int32_t>(c->meta_pf);
                 HIPTRY(c, hipMemcpyAsync(mp + kMetaActive, &nsel, 4, hipMemcpyHostToDevice, c->stream));
-                rmsnorm(c->bf16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, nsel,
+                rmsnorm(c->f16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, nsel,
                         c->g_out, c->m.rms_eps, c->d, c->hb.p, c->stream);
-                gemm_logits(c->bf16, c->hb.p, c->d, c->w_lm, c->V, c->d, mp + kMetaActive, nsel,
+                gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d, mp + kMetaActive, nsel,
                             as<float>(c->score_logits), c->b_lm, c->stream);
                 HIPTRY(c, hipGetLastError());
             }

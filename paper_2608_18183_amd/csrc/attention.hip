@@ -4,9 +4,9 @@
 // keys 0..pos0+i, which the QKV epilogue has already written (the window's own
 // keys included).
 //
-// bf16 path (head_dim 64): one workgroup per (segment, query block, head); the
+// fp16 path (head_dim 64): one workgroup per (segment, query block, head); the
 // four wavefronts split the 64-key tiles (= KV pages) round-robin by absolute
-// tile index and run an online softmax on v_mfma_f32_16x16x32_bf16 with the
+// tile index and run an online softmax on v_mfma_f32_16x16x32_f16 with the
 // scores computed transposed, S^T = K Q^T: lane (g, c16) then owns query
 // column c16 of each 16-query block, so the softmax needs only a two-step
 // exchange across the four lane groups per block, and the probabilities are
@@ -20,15 +20,15 @@
 
 namespace hbsjd {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
-__device__ inline bf16x8_t load_bf16x8(const uint16_t* p) {
-    return *reinterpret_cast<const bf16x8_t*>(p);
+__device__ inline f16x8_t load_f16x8(const uint16_t* p) {
+    return *reinterpret_cast<const f16x8_t*>(p);
 }
 
 template <int NMT>
-__global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ qb,
+__global__ __launch_bounds__(256) void k_attn_f16(const uint16_t* __restrict__ qb,
                                                    uint16_t* __restrict__ ob, int d, int H,
                                                    const uint16_t* __restrict__ kv, int maxp,
                                                    Segments seg, const int* __restrict__ nseg_dev,
@@ -62,15 +62,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
 
     // Q as the B operand: lane (g, c16) holds query c16 + 16 i, dims 32 kk + 8 g ..
     // (rows past the segment load its last row and are zeroed)
-    bf16x8_t qf[NMT][2];
+    f16x8_t qf[NMT][2];
 #pragma unroll
     for (int i = 0; i < NMT; ++i) {
         const int r = i * 16 + c16;
         const int rr = min(r, nq - 1);
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            const bf16x8_t x = load_bf16x8(qb + (size_t)(row0 + rr) * d + head * 64 + kk * 32 + 8 * g);
-            qf[i][kk] = r < nq ? x : bf16x8_t{};
+            const f16x8_t x = load_f16x8(qb + (size_t)(row0 + rr) * d + head * 64 + kk * 32 + 8 * g);
+            qf[i][kk] = r < nq ? x : f16x8_t{};
         }
     }
     // O^T accumulators (dims dj*16 + 4 g + v of query c16 + 16 i), the column's
@@ -98,13 +98,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         const uint16_t* Vb = kv + (size_t)page * page_elems + (size_t)(H + head) * 4096;
         // both operands of the tile are fetched before any MFMA so their
         // latencies overlap
-        bf16x8_t kf[4][2], vf[4][2];
+        f16x8_t kf[4][2], vf[4][2];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int kd = 0; kd < 2; ++kd) {
-                kf[j][kd] = load_bf16x8(Kb + (32 * (j >> 1) + 4 * (j & 1) + krow) * 64 + kd * 32 + 8 * g);
-                vf[j][kd] = load_bf16x8(Vb + (j * 16 + c16) * 64 + kd * 32 + 8 * g);
+                kf[j][kd] = load_f16x8(Kb + (32 * (j >> 1) + 4 * (j & 1) + krow) * 64 + kd * 32 + 8 * g);
+                vf[j][kd] = load_f16x8(Vb + (j * 16 + c16) * 64 + kd * 32 + 8 * g);
             }
         f32x4_t s[NMT][4];
 #pragma unroll
@@ -115,7 +115,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
             for (int kd = 0; kd < 2; ++kd)
 #pragma unroll
                 for (int i = 0; i < NMT; ++i)
-                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[j][kd], qf[i][kd], s[i][j],
+                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[j][kd], qf[i][kd], s[i][j],
                                                                       0, 0, 0);
         }
         // online softmax of each query column over the tile's 64 keys
@@ -159,15 +159,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
             for (int i = 0; i < NMT; ++i) {
-                bf16x8_t pf;
+                f16x8_t pf;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    pf[e] = (__bf16)s[i][2 * kk][e];
-                    pf[4 + e] = (__bf16)s[i][2 * kk + 1][e];
+                    pf[e] = (_Float16)s[i][2 * kk][e];
+                    pf[4 + e] = (_Float16)s[i][2 * kk + 1][e];
                 }
 #pragma unroll
                 for (int dj = 0; dj < 4; ++dj)
-                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dj][kk], pf, o[i][dj],
+                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[dj][kk], pf, o[i][dj],
                                                                        0, 0, 0);
             }
     }
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(const uint16_t* __restrict__ 
         }
         float a = sc[0] * lds[lane * LS + r];
         for (int ww = 1; ww < 4; ++ww) a += sc[ww] * lds[ww * 64 * LS + lane * LS + r];
-        ob[(size_t)(row0 + r) * d + head * 64 + lane] = f32_to_bf16(a / lt);
+        ob[(size_t)(row0 + r) * d + head * 64 + lane] = f32_to_f16_rne(a / lt);
     }
 }
 
@@ -257,19 +257,19 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
     }
 }
 
-void attention(bool bf16, const void* q, void* o, int d, int heads, int head_dim,
+void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
                const void* kv_layer, const int32_t* ptab, int max_pages, const Segments& seg,
                const int* nseg_dev, int nseg_cap, int max_rows_per_seg, const RowMeta& rows,
                const int* nrows_dev, int nrows_cap, hipStream_t s) {
-    if (bf16) {
+    if (f16) {
         if (nseg_cap <= 0) return;
         if (max_rows_per_seg <= 16) {
-            launch(k_attn_bf16<1>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
+            launch(k_attn_f16<1>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
                    (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, 1);
         } else {
             // 32 query rows per block; long (prefill) segments split into several
             const int qblocks = (max_rows_per_seg + 31) / 32;
-            launch(k_attn_bf16<2>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
+            launch(k_attn_f16<2>, dim3(nseg_cap * qblocks, heads), dim3(256), 0, s,
                    (const uint16_t*)q, (uint16_t*)o, d, heads, (const uint16_t*)kv_layer,
                    max_pages, seg, nseg_dev, qblocks);
         }

@@ -38,7 +38,13 @@ enum DeviceError : int {
     kErrRoundOverflow = 8,
 };
 
-// ------------------------------------------------------------ bf16
+// ------------------------------------------------------------ 16-bit numbers
+// A bf16 model's weights are rounded to bf16 (nearest-even) on load. The MFMA
+// operands, the activations between kernels and the KV cache are fp16: the
+// same operand width and matrix-core rate as bf16, with three more mantissa
+// bits. Each weight matrix is held as fp16 times a power of two (its scale), so
+// every bf16 weight of the matrix down to 2^-31 of its largest magnitude is
+// represented exactly; the GEMMs multiply their fp32 sums by the inverse scale.
 
 __host__ __device__ inline uint16_t f32_to_bf16(float f) {
     uint32_t u;
@@ -55,17 +61,43 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
     return f;
 }
 
+// fp32 -> fp16 bits, round to nearest even, for the host's weight conversion
+// (finite inputs whose magnitude is below 65520; larger ones give infinity)
+inline uint16_t f32_to_f16_bits_host(float f) {
+    uint32_t u;
+    __builtin_memcpy(&u, &f, 4);
+    const uint16_t sign = (uint16_t)((u >> 16) & 0x8000u);
+    const int e = (int)((u >> 23) & 0xFF) - 127;
+    uint32_t m = u & 0x7FFFFFu;
+    if (e > 15) return sign | 0x7C00u;
+    if (e >= -14) {   // normal: keep 10 of the 23 mantissa bits
+        uint32_t h = ((uint32_t)(e + 15) << 10) | (m >> 13);
+        const uint32_t rest = m & 0x1FFFu;
+        if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) ++h;   // may carry into the exponent
+        return sign | (uint16_t)h;
+    }
+    if (e < -25) return sign;   // below half the smallest subnormal
+    // subnormal: value = m' * 2^-24 with m' = (1.m) * 2^(e + 24)
+    m |= 0x800000u;
+    const int shift = -e - 1;   // 14 .. 24: bits of the 24-bit significand dropped
+    uint32_t h = m >> shift;
+    const uint32_t rest = m & ((1u << shift) - 1u), half = 1u << (shift - 1);
+    if (rest > half || (rest == half && (h & 1u))) ++h;
+    return sign | (uint16_t)h;
+}
+
+// device conversions use the hardware converts (round to nearest even)
+__device__ inline uint16_t f32_to_f16_rne(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+__device__ inline float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
     __device__ static float load(const float* p) { return *p; }
     __device__ static void store(float* p, float v) { *p = v; }
 };
-// the device conversion uses the hardware's round-to-nearest-even convert;
-// it agrees with f32_to_bf16 on every finite value
-__device__ inline uint16_t f32_to_bf16_rne(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 template <> struct Elem<uint16_t> {
-    __device__ static float load(const uint16_t* p) { return bf16_to_f32(*p); }
-    __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
+    __device__ static float load(const uint16_t* p) { return f16_to_f32(*p); }
+    __device__ static void store(uint16_t* p, float v) { *p = f32_to_f16_rne(v); }
 };
 
 // ------------------------------------------------------------ Philox4x32-10

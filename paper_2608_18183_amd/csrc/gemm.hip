@@ -3,11 +3,12 @@
 // fused into the epilogue (2D RoPE and the paged KV append after QKV, the
 // residual add after O and W2, SwiGLU after W1|W3, bias after the lm_head).
 //
-// bf16 path: 256-thread workgroups, 2x2 wavefronts, LDS-staged 64-deep K
-// tiles with an XOR swizzle (loaded straight into LDS for the 64x64 tile,
-// through registers for the 128x128 one), v_mfma_f32_16x16x32_bf16 with fp32
-// accumulation. An output element sums its K range in the same order wherever
-// its row sits in the launch, and for the unsplit projections (QKV, W1|W3,
+// fp16 path (the bf16 model's weights held as scaled fp16, fp16 activations):
+// 256-thread workgroups, 2x2 wavefronts, LDS-staged 64-deep K tiles with an
+// XOR swizzle (loaded straight into LDS for the 64x64 tile, through registers
+// for the 128x128 one), v_mfma_f32_16x16x32_f16 with fp32 accumulation, the
+// sums multiplied by the weights' inverse scale before the epilogue. An output
+// element sums its K range in the same order wherever its row sits in the launch, and for the unsplit projections (QKV, W1|W3,
 // lm_head) whatever the launch's size or tile. O and W2 cut K into as many
 // parts as split_for gives for the launch's row capacity, so there the order
 // of the partial sums, and a row's last bits, follow that capacity.
@@ -17,7 +18,7 @@
 
 namespace hbsjd {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 // 16-byte staging chunk as a first-class vector (a copy of HIP's uint4 struct
 // becomes a memcpy that keeps the stage arrays out of registers)
@@ -26,7 +27,7 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 // ---------------------------------------------------------------- epilogues
 // operator()(row, col, value, value of column col ^ 1 in the same row)
 
-// The bf16 kernel calls begin_tile(n0) once, row_info(m) once per output row
+// The fp16 kernel calls begin_tile(n0) once, row_info(m) once per output row
 // and operator()(info, m, n, value, partner) per element; the fp32 kernel only
 // uses the last two.
 
@@ -40,7 +41,7 @@ struct EpiQkv {
     const float* rs;
     int d, heads, dh, T_;
     int part = 0;   // 0 q, 1 k, 2 v: fixed per tile since d is a multiple of the tile width
-    // the bf16 path has head_dim 64; the fp32 path takes it at run time
+    // the fp16 path has head_dim 64; the fp32 path takes it at run time
     static constexpr int kDh = sizeof(T) == 2 ? 64 : 0;
     // the RoPE factors are fetched after the main loop: holding them through it
     // costs more (register pressure) than the one exposed load
@@ -88,8 +89,8 @@ struct EpiQkv {
         const int col = part == 0 ? c : part == 1 ? head * 64 * dhv + e : head * 64 * dhv + e * 64;
         Elem<T>::store((part == 0 ? q : kv) + (ri.off + col), out);
     }
-    // bf16 square tiles of BT = 64 or 128 columns (BT / 64 heads of one part)
-    // are staged in LDS as bf16, tile[r * tile_ld<BT>() + c], and written from
+    // fp16 square tiles of BT = 64 or 128 columns (BT / 64 heads of one part)
+    // are staged in LDS as fp16, tile[r * tile_ld<BT>() + c], and written from
     // there: q and K rows as 16-byte chunks (eight lanes per head row), V^T one
     // row (= cache slot) per lane, so a wavefront's store covers consecutive
     // slots of one dimension instead of 16 dimensions of 4 rows
@@ -99,7 +100,7 @@ struct EpiQkv {
     // element (rl, cl) of the tile (local row and column), global column n
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux& ax, int n, float v,
                           float partner) const {
-        tile[rl * ld + cl] = f32_to_bf16_rne(value(ax, n, v, partner));
+        tile[rl * ld + cl] = f32_to_f16_rne(value(ax, n, v, partner));
     }
     template <int BT>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
@@ -176,7 +177,7 @@ struct EpiSwiGLU {
         if (n & 1) return;
         Elem<T>::store(act + (size_t)m * ld + (n >> 1), swiglu(v, partner));
     }
-    // bf16 square tiles of BT columns give BT rows of BT / 2 outputs, staged
+    // fp16 square tiles of BT columns give BT rows of BT / 2 outputs, staged
     // in LDS and written as 16-byte chunks per row. Only the 64x64 tile uses
     // it: at 128x128 the staging measured slower than storing from registers
     // (stress rounds 48 -> 53 us per launch)
@@ -185,7 +186,7 @@ struct EpiSwiGLU {
     __device__ int tile_ld() const { return BT / 2 + 8; }
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux&, int, float v,
                           float partner) const {
-        if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_bf16_rne(swiglu(v, partner));
+        if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_f16_rne(swiglu(v, partner));
     }
     template <int BT>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
@@ -224,7 +225,7 @@ struct EpiLogits {
     __device__ void operator()(int m, int n, float v, float p) const { (*this)(Row{}, m, n, v, p); }
 };
 
-// ---------------------------------------------------------------- bf16 MFMA
+// ---------------------------------------------------------------- fp16 MFMA
 // Workgroup tile BM x BN, 4 wavefronts arranged WGM x WGN, 64-deep K steps,
 // operands in LDS as rows of eight 16-byte chunks, chunk c of row r stored at
 // position c ^ (r & 7) so the MFMA operand reads fall in distinct banks.
@@ -260,7 +261,7 @@ template <typename E>
 constexpr auto epi_prefetches_aux(int) -> decltype(E::kLateAux, bool()) { return !E::kLateAux; }
 template <typename E>
 constexpr bool epi_prefetches_aux(long) { return true; }
-// an epilogue may stage a square bf16 tile in LDS and store it itself
+// an epilogue may stage a square fp16 tile in LDS and store it itself
 // (static constexpr bool stores_tile(int tile width); stage(), store_tile())
 template <typename E>
 constexpr auto epi_stores_tile(int bt) -> decltype(E::stores_tile(0), bool()) {
@@ -286,10 +287,11 @@ __device__ __forceinline__ void wait_loads() {
 }
 
 template <int BM, int BN, int WGM, int WGN, int NS, bool kDirect, typename Epi>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ A, int lda,
-                                                   const uint16_t* __restrict__ W, int N, int K,
-                                                   const int* __restrict__ m_dev, int m_cap,
-                                                   int splits, float* __restrict__ part, Epi epi) {
+__global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A, int lda,
+                                                  const uint16_t* __restrict__ W, float wscale,
+                                                  int N, int K, const int* __restrict__ m_dev,
+                                                  int m_cap, int splits, float* __restrict__ part,
+                                                  Epi epi) {
     constexpr int BK = 64;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 16, TN = WN / 16;
@@ -330,22 +332,22 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             const int ch = kk * 4 + (lane >> 4);
-            bf16x8_t af[TM], bfr[TN];
+            f16x8_t af[TM], bfr[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int r = wm * WM + i * 16 + (lane & 15);
-                af[i] = *reinterpret_cast<const bf16x8_t*>(&As[r * BK + ((ch ^ (r & 7)) << 3)]);
+                af[i] = *reinterpret_cast<const f16x8_t*>(&As[r * BK + ((ch ^ (r & 7)) << 3)]);
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int r = wn * WN + j * 16 + (lane & 15);
-                bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[r * BK + ((ch ^ (r & 7)) << 3)]);
+                bfr[j] = *reinterpret_cast<const f16x8_t*>(&Bs[r * BK + ((ch ^ (r & 7)) << 3)]);
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j],
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[i], bfr[j], acc[i][j],
                                                                         0, 0, 0);
         }
     };
@@ -491,6 +493,12 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
         }
     }
 
+    // the weights are held scaled by a power of two: undo it (exact)
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] *= wscale;
+
     // 16x16 accumulator layout: lane holds rows 4*(lane/16)+v of column lane%16
     if (part) {
         float* P = part + (size_t)z * m_cap * N;
@@ -554,38 +562,43 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ 
 }
 
 template <int BM, int BN, int WGM, int WGN, typename Epi>
-static void launch_bf16(const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-                        int m_cap, int splits, float* part, const Epi& epi, hipStream_t s) {
+static void launch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
+                       const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
+                       hipStream_t s) {
     if (m_cap <= 0) return;
     const int tiles = ((m_cap + BM - 1) / BM) * (N / BN) * splits;
     const int grid = ((tiles + 7) / 8) * 8;
     if constexpr (BM * BN >= 128 * 128) {
         // the large tiles have enough MFMA work per step to cover a shallow
         // register pipeline (direct staging measured no faster there)
-        launch(k_gemm_bf16<BM, BN, WGM, WGN, 3, false, Epi>, dim3(grid), dim3(256), 0, s,
-               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+        launch(k_gemm_f16<BM, BN, WGM, WGN, 3, false, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
+               part, epi);
     } else if (tiles <= 512) {
         // direct staging, 4 stages (64 KB of LDS): two workgroups per CU hold
         // the whole launch
-        launch(k_gemm_bf16<BM, BN, WGM, WGN, 4, true, Epi>, dim3(grid), dim3(256), 0, s,
-               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+        launch(k_gemm_f16<BM, BN, WGM, WGN, 4, true, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
+               part, epi);
     } else {
         // more tiles than two per CU: 3 stages (48 KB), three workgroups per CU
-        launch(k_gemm_bf16<BM, BN, WGM, WGN, 3, true, Epi>, dim3(grid), dim3(256), 0, s,
-               (const uint16_t*)A, lda, (const uint16_t*)W, N, K, m_dev, m_cap, splits, part, epi);
+        launch(k_gemm_f16<BM, BN, WGM, WGN, 3, true, Epi>, dim3(grid), dim3(256), 0, s,
+               (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
+               part, epi);
     }
 }
 
 // tile choice by the launch's row cap (the same for Full and Compact rounds):
 // large tiles once there are enough of them to fill the 256 CUs twice over
 template <typename Epi>
-static void dispatch_bf16(const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-                          int m_cap, int splits, float* part, const Epi& epi, hipStream_t s) {
+static void dispatch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
+                         const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
+                         hipStream_t s) {
     const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
     if (N % 128 == 0 && t128 >= 512)
-        launch_bf16<128, 128, 2, 2>(A, lda, W, N, K, m_dev, m_cap, splits, part, epi, s);
+        launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
     else
-        launch_bf16<64, 64, 2, 2>(A, lda, W, N, K, m_dev, m_cap, splits, part, epi, s);
+        launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
 }
 
 // ---------------------------------------------------------------- fp32
@@ -663,12 +676,12 @@ int split_for(int m_cap, int N, int K) {
     return sp;
 }
 
-void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-              int m_cap, const QkvArgs& e, hipStream_t s) {
-    if (bf16) {
+void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
+              const int* m_dev, int m_cap, const QkvArgs& e, hipStream_t s) {
+    if (f16) {
         EpiQkv<uint16_t> epi{(uint16_t*)e.q, (uint16_t*)e.kv, e.pos, e.kvslot, e.rope_cos,
                              e.rope_sin, e.d, e.heads, e.head_dim, e.T};
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s);
     } else {
         EpiQkv<float> epi{(float*)e.q, (float*)e.kv, e.pos, e.kvslot, e.rope_cos, e.rope_sin,
                           e.d, e.heads, e.head_dim, e.T};
@@ -680,9 +693,10 @@ template <int Tag>   // 0 the O projection, 1 W2 (distinct kernel names in trace
 struct PartialTag {};
 
 template <int Tag>
-static void partial_tag(bool bf16, const void* A, int lda, const void* W, int N, int K,
-                        const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
-    if (bf16) {
+static void partial_tag(bool f16, const void* A, int lda, const void* W, float wscale, int N,
+                        int K, const int* m_dev, int m_cap, int splits, float* part,
+                        hipStream_t s) {
+    if (f16) {
         struct EpiNone {
             struct Row {};
             struct Aux {};
@@ -692,43 +706,43 @@ static void partial_tag(bool bf16, const void* A, int lda, const void* W, int N,
             __device__ void store(const Row&, const Aux&, int, int, float, float) const {}
             PartialTag<Tag> tag;
         };
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, splits, part, EpiNone{}, s);
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, EpiNone{}, s);
     } else {
         launch_f32(A, lda, W, N, K, m_dev, m_cap, EpiStore{part, N}, s);
     }
 }
 
-void gemm_partial(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
-                  const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
+void gemm_partial(bool f16, int tag, const void* A, int lda, const void* W, float wscale, int N,
+                  int K, const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
     if (tag == 0)
-        partial_tag<0>(bf16, A, lda, W, N, K, m_dev, m_cap, splits, part, s);
+        partial_tag<0>(f16, A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, s);
     else
-        partial_tag<1>(bf16, A, lda, W, N, K, m_dev, m_cap, splits, part, s);
+        partial_tag<1>(f16, A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, s);
 }
 
-void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
+void gemm_swiglu(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s) {
-    if (bf16) {
+    if (f16) {
         EpiSwiGLU<uint16_t> epi{(uint16_t*)act, N / 2};
-        dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s);
     } else {
         EpiSwiGLU<float> epi{(float*)act, N / 2};
         launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
     }
 }
 
-void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
+void gemm_logits(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
                  const int* m_dev, int m_cap, float* out, const float* bias, hipStream_t s) {
     if (bias) {
         EpiLogits<true> epi{out, bias, N};
-        if (bf16)
-            dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        if (f16)
+            dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s);
         else
             launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
     } else {
         EpiLogits<false> epi{out, nullptr, N};
-        if (bf16)
-            dispatch_bf16(A, lda, W, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        if (f16)
+            dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s);
         else
             launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
     }

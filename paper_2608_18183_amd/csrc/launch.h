@@ -71,33 +71,37 @@ struct QkvArgs {
     int d, heads, head_dim, T;
 };
 
-void gemm_qkv(bool bf16, const void* A, int lda, const void* W, int N, int K, const int* m_dev,
-              int m_cap, const QkvArgs& e, hipStream_t s);
+// With f16, A and W are fp16 and the sums are multiplied by wscale (the
+// inverse of the power-of-two scale the weights are held with); the fp32 path
+// ignores wscale.
+void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
+              const int* m_dev, int m_cap, const QkvArgs& e, hipStream_t s);
 // split-K partial sums part[split][m_cap][N] (tag 0: O projection, 1: W2);
 // split_for() is the split count the host must size `part` for
 int split_for(int m_cap, int N, int K);
-void gemm_partial(bool bf16, int tag, const void* A, int lda, const void* W, int N, int K,
-                  const int* m_dev, int m_cap, int splits, float* part, hipStream_t s);
-void gemm_swiglu(bool bf16, const void* A, int lda, const void* W, int N, int K,
+void gemm_partial(bool f16, int tag, const void* A, int lda, const void* W, float wscale, int N,
+                  int K, const int* m_dev, int m_cap, int splits, float* part, hipStream_t s);
+void gemm_swiglu(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s);
-void gemm_logits(bool bf16, const void* A, int lda, const void* W, int N, int K,
+void gemm_logits(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
                  const int* m_dev, int m_cap, float* out, const float* bias, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
-void attention(bool bf16, const void* q, void* o, int d, int heads, int head_dim,
+void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
                const void* kv_layer, const int32_t* ptab, int max_pages, const Segments& seg,
                const int* nseg_dev, int nseg_cap, int max_rows_per_seg, const RowMeta& rows,
                const int* nrows_dev, int nrows_cap, hipStream_t s);
 
 // ---------------------------------------------------------------- row ops
-void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
-                const void* tok_emb, const void* cls_emb, const float* gain, float eps, int d,
+// the embedding tables are fp32 on both paths
+void embed_norm(bool f16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
+                const float* tok_emb, const float* cls_emb, const float* gain, float eps, int d,
                 float* h, void* hb, hipStream_t s);
-void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
+void rmsnorm(bool f16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s);
 // h += sum over splits (in split order) of part[split][m_cap][d]; then
 // hb = RMSNorm(h) * gain (hb may be null)
-void reduce_residual_norm(bool bf16, const float* part, int splits, int m_cap, float* h,
+void reduce_residual_norm(bool f16, const float* part, int splits, int m_cap, float* h,
                           const int* nrows_dev, const float* gain, float eps, int d, void* hb,
                           hipStream_t s);
 

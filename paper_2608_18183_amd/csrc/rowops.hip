@@ -194,8 +194,8 @@ void check_prefix(const int32_t* prefix, const int32_t* len, int B, int T, int V
 constexpr int kMaxPer = 24;   // d <= 1536
 
 // Every global load of these kernels is unconditional (lanes past d re-read
-// entry d - 1 and zero it afterwards) and raw: a bf16 value converted inside a
-// guarded block makes the compiler wait for each load before the next one.
+// entry d - 1 and zero it afterwards): a load inside a guarded block makes the
+// compiler wait for each load before the next one.
 template <int PER>
 __device__ inline void load_gain(const float* __restrict__ g, int d, float (&gv)[PER]) {
     const int lane = threadIdx.x & 63;
@@ -219,20 +219,10 @@ __device__ inline void norm_store(const float (&x)[PER], const float (&gv)[PER],
     }
 }
 
-template <typename T> struct Raw;
-template <> struct Raw<float> {
-    using type = float;
-    __device__ static float f32(float v) { return v; }
-};
-template <> struct Raw<uint16_t> {
-    using type = uint16_t;
-    __device__ static float f32(uint16_t v) { return bf16_to_f32(v); }
-};
-
 template <typename T, int PER>
 __global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nrows_dev, int cap,
-                                                    const T* __restrict__ tok_emb,
-                                                    const T* __restrict__ cls_emb,
+                                                    const float* __restrict__ tok_emb,
+                                                    const float* __restrict__ cls_emb,
                                                     const float* __restrict__ g, float eps, int d,
                                                     float* __restrict__ h, T* __restrict__ hb) {
     const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -244,13 +234,13 @@ __global__ __launch_bounds__(256) void k_embed_norm(RowMeta rows, const int* nro
     const int nrows = *nrows_dev;
     const int tok = rows.tok[r];
     if (r >= nrows) return;
-    const T* e = tok >= 0 ? tok_emb + (size_t)tok * d : cls_emb + (size_t)(-(tok + 1)) * d;
-    typename Raw<T>::type raw[PER];
-#pragma unroll
-    for (int k = 0; k < PER; ++k) raw[k] = e[min(lane + 64 * k, d - 1)];
+    const float* e = tok >= 0 ? tok_emb + (size_t)tok * d : cls_emb + (size_t)(-(tok + 1)) * d;
     float x[PER];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) x[k] = lane + 64 * k < d ? Raw<T>::f32(raw[k]) : 0.f;
+    for (int k = 0; k < PER; ++k) x[k] = e[min(lane + 64 * k, d - 1)];
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+        if (lane + 64 * k >= d) x[k] = 0.f;
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
         const int i = lane + 64 * k;
@@ -280,7 +270,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h,
     norm_store<T, PER>(x, gv, eps, d, hb + (size_t)r * d);
 }
 
-// the per-lane element count of a row of d (a multiple of 64 in bf16 mode)
+// the per-lane element count of a row of d (a multiple of 64 in fp16 mode)
 template <typename F>
 static void by_per(int d, F f) {
     const int per = (d + 63) / 64;
@@ -292,30 +282,29 @@ static void by_per(int d, F f) {
     else f(std::integral_constant<int, 24>{});
 }
 
-void embed_norm(bool bf16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
-                const void* tok_emb, const void* cls_emb, const float* gain, float eps, int d,
+void embed_norm(bool f16, const RowMeta& rows, const int* nrows_dev, int nrows_cap,
+                const float* tok_emb, const float* cls_emb, const float* gain, float eps, int d,
                 float* h, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     const dim3 grid((nrows_cap + 3) / 4);
     by_per(d, [&](auto P) {
         constexpr int PER = decltype(P)::value;
-        if (bf16)
+        if (f16)
             launch(k_embed_norm<uint16_t, PER>, grid, dim3(256), 0, s, rows, nrows_dev, nrows_cap,
-                   (const uint16_t*)tok_emb, (const uint16_t*)cls_emb, gain, eps, d, h,
-                   (uint16_t*)hb);
+                   tok_emb, cls_emb, gain, eps, d, h, (uint16_t*)hb);
         else
             launch(k_embed_norm<float, PER>, grid, dim3(256), 0, s, rows, nrows_dev, nrows_cap,
-                   (const float*)tok_emb, (const float*)cls_emb, gain, eps, d, h, (float*)hb);
+                   tok_emb, cls_emb, gain, eps, d, h, (float*)hb);
     });
 }
 
-void rmsnorm(bool bf16, const float* h, const int32_t* src_idx, const int* nrows_dev,
+void rmsnorm(bool f16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s) {
     if (nrows_cap <= 0) return;
     const dim3 grid((nrows_cap + 3) / 4);
     by_per(d, [&](auto P) {
         constexpr int PER = decltype(P)::value;
-        if (bf16)
+        if (f16)
             launch(k_rmsnorm<uint16_t, PER>, grid, dim3(256), 0, s, h, src_idx, nrows_dev,
                    nrows_cap, gain, eps, d, (uint16_t*)hb);
         else
@@ -416,11 +405,11 @@ static void reduce_norm_dispatch(const float* part, int splits, int m_cap, float
     }
 }
 
-void reduce_residual_norm(bool bf16, const float* part, int splits, int m_cap, float* h,
+void reduce_residual_norm(bool f16, const float* part, int splits, int m_cap, float* h,
                           const int* nrows_dev, const float* gain, float eps, int d, void* hb,
                           hipStream_t s) {
     if (m_cap <= 0) return;
-    if (bf16)
+    if (f16)
         reduce_norm_dispatch<uint16_t>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);
     else
         reduce_norm_dispatch<float>(part, splits, m_cap, h, nrows_dev, gain, eps, d, hb, s);

@@ -5,9 +5,9 @@ fp32 oracle one for one, so these check what holds at any size:
   * every round commits 1..min(W, T - n) tokens and the counts sum to T - k;
   * prefixes are kept and every token is in the vocabulary;
   * Full, Compact and AUTO execution give the same tokens (Sec. 4.3);
-and, on sampled sequences of the rollout (B, stress and L shapes), that the
+and, on sampled sequences of the rollout (B, stress, L and XL shapes), that the
 oracle's logits match the GPU forward (3e-2 max-abs / 1e-2 mean-abs) and every
-generated token lies in the oracle's top-k support (with a 5% margin for bf16
+generated token lies in the oracle's top-k support (with a 5% margin for
 rounding at the edge)."""
 import numpy as np
 import pytest
@@ -142,13 +142,37 @@ def test_full_size_l_shape_forward_and_rollout():
     assert rank.max() <= int(wl.top_k * 1.05), (b, rank.max())
 
 
-def test_full_size_xl_cfg_rollout_invariants():
+def test_full_size_xl_cfg_rollout_invariants_and_samples():
+    """The XL workload with guidance (256 verifier row sets of W + 1 rows):
+    invariants, AUTO = Compact, and on the image with the shortest prefix the
+    oracle's conditional and null-class logits of its first 96 generated
+    positions against the GPU forward (3e-2 / 1e-2), with every token it drew
+    inside the top-k support of the oracle's guided logits (Sec. 4.2: CFG
+    branches verify on the fused guided logits)."""
     wl, shape, blob, batch, ctx = _setup("llamagen_xl_cfg")
     ctx.hbsjd_calibrate_gamma(wl.batch, wl.window)
     out = _rollout(ctx, wl, batch, 1000, P().EXEC_AUTO)
-    t = _check_invariants(out, batch, wl, shape.T, shape.vocab)
+    tok = _check_invariants(out, batch, wl, shape.T, shape.vocab)
     comp = _rollout(ctx, wl, batch, 1000, P().EXEC_COMPACT)
-    assert np.array_equal(comp["tokens"].cpu().numpy(), t)
+    assert np.array_equal(comp["tokens"].cpu().numpy(), tok)
+    b = int(np.argmin(batch.prefix_len))
+    k = int(batch.prefix_len[b])
+    n = min(shape.T - 1, k + 96)                 # positions 0..n: predictions of 1..n+1
+    labels = [int(batch.labels[b]), shape.n_classes]
+    om = oracle.Model(shape, gu.bf16_rounded_blob(shape, blob))
+    ref = om.forward_batch(labels, [tok[b, :n], tok[b, :n]])
+    dev = np.zeros((2, shape.T), dtype=np.int32)
+    dev[:, :n] = tok[b, :n]
+    got = ctx.hbsjd_forward(torch.from_numpy(dev).cuda(), [n, n], labels).cpu().numpy()
+    got = got.reshape(2, n + 1, shape.vocab)
+    for j in range(2):
+        err = np.abs(got[j].astype(np.float64) - ref[j])
+        assert err.max() <= 3e-2 and err.mean() <= 1e-2, (j, err.max(), err.mean())
+    lc, lu = ref[0][k:n + 1], ref[1][k:n + 1]
+    y = (lu + wl.cfg_scale * (lc - lu)) / float(batch.temperature[b])
+    drawn = tok[b, k:n + 1]
+    rank = (y > y[np.arange(len(drawn)), drawn][:, None]).sum(axis=1) + 1
+    assert rank.max() <= int(wl.top_k * 1.05), (b, rank.max())
 
 
 def test_full_size_sync_schedule():

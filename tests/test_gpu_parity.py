@@ -3,7 +3,8 @@ same seeded inputs.
 
 Bars: bit-exact for the RNG, the verification kernel on identical fp32 rows and
 uniforms, and the fp32-mode rollout tokens; 3e-2 max-abs / 1e-2 mean-abs for
-bf16 logits against the fp32 oracle run on the same bf16-rounded weights."""
+the logits of a bf16 model (fp16 operands and activations on the GPU) against
+the fp32 oracle run on the same bf16-rounded weights."""
 import numpy as np
 import pytest
 
@@ -127,15 +128,8 @@ def test_forward_bf16_stress_shape_with_bias_matches_oracle():
     _bf16_forward_case("stress_b", [200, 3], 2)
 
 
-@pytest.mark.xfail(reason="36 layers of bf16 activation rounding reach 0.03-0.04 max-abs "
-                   "(mean 0.005); the 3e-2 max-abs bar is not met at this depth yet",
-                   strict=False)
 def test_forward_bf16_llamagen_xl_matches_oracle():
-    _bf16_forward_case("llamagen_xl_cfg", [40, 0], 3)
-
-
-def test_forward_bf16_llamagen_xl_mean_error():
-    _bf16_forward_case("llamagen_xl_cfg", [40, 0], 3, atol_max=6e-2)
+    _bf16_forward_case("llamagen_xl_cfg", [40, 0, 90], 3)
 
 
 @pytest.mark.parametrize("n_seq", [12, 44])
