@@ -292,6 +292,24 @@ hbsjd_status hbsjd_transform_rows(int32_t rows, int32_t V, const float* logits, 
                                   int32_t* argmax, int32_t* draw, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * hbsjd_transform_rows with the same arguments, results and errors, whose
+ * per-row metadata lives in a fixed library-owned device array (8 bytes per
+ * row plus 64; each GPU the library runs on keeps its copy until the process
+ * ends) instead of an allocation per call. It allocates and frees nothing.
+ * rows <= HBSJD_NOALLOC_MAX_ROWS, EINVAL beyond. Every call on one GPU uses
+ * that GPU's one array: calls that overlap on the same GPU (from several host
+ * threads, or queued on several streams without ordering between them) race
+ * and give undefined results.
+ */
+#define HBSJD_NOALLOC_MAX_ROWS 65536
+hbsjd_status hbsjd_transform_rows_noalloc(int32_t rows, int32_t V, const float* logits,
+                                          int32_t cfg, float cfg_scale, const float* temperature,
+                                          int32_t top_k, uint64_t seed, const int32_t* position,
+                                          float* p, int32_t* argmax, int32_t* draw, void* stream);
+
+/*
  * The verification kernel (Sec. 4.2, Eq. 5) on caller-supplied rows, for
  * testing; the acceptance test and the replacement draw are the rollout's own
  * code. All pointers are device memory: p and q fp32 [B][W][V] (target and

@@ -67,6 +67,8 @@ _SIGS = {
     "hbsjd_verify_probs": (_I32, [_I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),
     "hbsjd_transform_rows": (_I32, [_I32, _I32, _P, _I32, ctypes.c_float, _P, _I32,
                                     ctypes.c_uint64, _P, _P, _P, _P, _P]),
+    "hbsjd_transform_rows_noalloc": (_I32, [_I32, _I32, _P, _I32, ctypes.c_float, _P, _I32,
+                                            ctypes.c_uint64, _P, _P, _P, _P, _P]),
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
     "hbsjd_profile_start": (_I32, [_P, ctypes.c_uint32]),
@@ -319,11 +321,12 @@ def hbsjd_verify_probs(p, q, drafts, u_acc, u_res, stream=None):
 
 
 def hbsjd_transform_rows(logits, temperature, position, top_k: int = 0, cfg_scale: float = 0.0,
-                         seed: int = 0, stream=None, out=None):
+                         seed: int = 0, stream=None, out=None, noalloc: bool = False):
     """logits: fp32 device tensor [rows, V] or, with guidance, [rows, 2, V]
     (conditional then unconditional row); temperature fp32 and position int32
     device tensors [rows]. Returns (p [rows, V], argmax [rows], draw [rows])
-    device tensors, written into `out` when given."""
+    device tensors, written into `out` when given. noalloc=True calls
+    hbsjd_transform_rows_noalloc (no device allocation inside the library)."""
     import torch
     if logits.dim() == 2:
         rows, V = logits.shape
@@ -336,10 +339,11 @@ def hbsjd_transform_rows(logits, temperature, position, top_k: int = 0, cfg_scal
                torch.empty(rows, dtype=torch.int32, device=logits.device))
     p, amax, draw = out
     L = load_library()
-    _check(L.hbsjd_transform_rows(rows, V, _P(_dev_ptr(logits)), cfg, float(cfg_scale), _P(_dev_ptr(temperature)),
+    fn = L.hbsjd_transform_rows_noalloc if noalloc else L.hbsjd_transform_rows
+    _check(fn(rows, V, _P(_dev_ptr(logits)), cfg, float(cfg_scale), _P(_dev_ptr(temperature)),
               int(top_k), int(seed), _P(_dev_ptr(position)), _P(_dev_ptr(p)),
               _P(_dev_ptr(amax)), _P(_dev_ptr(draw)), _P(_stream_handle(stream))),
-           "hbsjd_transform_rows")
+           "hbsjd_transform_rows_noalloc" if noalloc else "hbsjd_transform_rows")
     return p, amax, draw
 
 

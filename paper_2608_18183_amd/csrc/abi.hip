@@ -18,6 +18,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1314,7 +1315,35 @@ hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
     }
 }
 
+// Fixed device workspace of hbsjd_transform_rows_noalloc: the per-row metadata
+// of up to HBSJD_NOALLOC_MAX_ROWS rows. Every GPU the library runs on holds its
+// own copy for the life of the process. Host code never passes this name to a
+// kernel or a copy (on the host it is only a stand-in for the symbol); it uses
+// the device address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) int32_t scratch[2 * HBSJD_NOALLOC_MAX_ROWS + kMetaCount];
+
 namespace {
+std::mutex g_scratch_mu;
+std::vector<int32_t*> g_scratch_ptr;   // per device: the address of its `scratch`
+
+// the current device's copy of `scratch`, looked up once per device
+hbsjd_status static_scratch(int32_t** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(HBSJD_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        g_scratch_ptr[dev] = static_cast<int32_t*>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return HBSJD_OK;
+}
+
 hbsjd_status check_transform_rows(int32_t rows, int32_t V, const float* logits, int32_t cfg,
                                   float cfg_scale, const float* temperature, int32_t top_k,
                                   const int32_t* position, const float* p, const int32_t* argmax,
@@ -1360,6 +1389,26 @@ hbsjd_status hbsjd_transform_rows(int32_t rows, int32_t V, const float* logits, 
         return st;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_transform_rows");
+    }
+}
+
+hbsjd_status hbsjd_transform_rows_noalloc(int32_t rows, int32_t V, const float* logits,
+                                          int32_t cfg, float cfg_scale, const float* temperature,
+                                          int32_t top_k, uint64_t seed, const int32_t* position,
+                                          float* p, int32_t* argmax, int32_t* draw, void* stream) {
+    try {
+        if (rows > HBSJD_NOALLOC_MAX_ROWS)
+            return fail(HBSJD_EINVAL, "rows exceeds HBSJD_NOALLOC_MAX_ROWS (65536)");
+        TRY(check_transform_rows(rows, V, logits, cfg, cfg_scale, temperature, top_k, position, p,
+                                 argmax, draw));
+        int32_t* ws = nullptr;
+        TRY(static_scratch(&ws));
+        hipStream_t s = (hipStream_t)stream;
+        transform_rows(rows, V, logits, cfg, cfg_scale, temperature, top_k, seed, position, p,
+                       argmax, draw, ws, s);
+        return finish_transform_rows(ws + 2 * (size_t)rows, s);
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_transform_rows_noalloc");
     }
 }
 
