@@ -266,6 +266,12 @@ void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
         if (max_rows_per_seg <= 16) {
             launch(k_attn_f16<1>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
                    (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, 1);
+        } else if (max_rows_per_seg > 32 && max_rows_per_seg <= 48) {
+            // a round window of 33..48 rows in one block, so the sequence's
+            // keys and values are read once per head (two 32-row blocks would
+            // each read them)
+            launch(k_attn_f16<3>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
+                   (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, 1);
         } else {
             // 32 query rows per block; long (prefill) segments split into several
             const int qblocks = (max_rows_per_seg + 31) / 32;

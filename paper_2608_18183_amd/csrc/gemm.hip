@@ -16,6 +16,17 @@
 #include "common.h"
 #include "launch.h"
 
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+
+// Elementwise epilogue arithmetic rounds every operation on its own (no fused
+// multiply-add contraction), so the wide-tile and the smaller-tile kernels,
+// whose epilogue code differs, give the same bits for the same row
+#pragma clang fp contract(off)
+
 namespace hbsjd {
 
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8_t;
@@ -30,6 +41,17 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 // The fp16 kernel calls begin_tile(n0) once, row_info(m) once per output row
 // and operator()(info, m, n, value, partner) per element; the fp32 kernel only
 // uses the last two.
+
+// 2D RoPE of one pair (x0, x1) = (element 2i, element 2i+1) of a head:
+// (x0 cos - x1 sin, x0 sin + x1 cos), each product rounded on its own (this
+// file compiles without contraction), so every kernel that applies it gets
+// the same bits
+__device__ __forceinline__ float rope_even(float x0, float x1, float cs, float sn) {
+    return x0 * cs - x1 * sn;
+}
+__device__ __forceinline__ float rope_odd(float x0, float x1, float cs, float sn) {
+    return x0 * sn + x1 * cs;
+}
 
 template <typename T>
 struct EpiQkv {
@@ -78,7 +100,7 @@ struct EpiQkv {
         const int dhv = head_dim();
         const int c = n - part * d;
         const int e = kDh ? c & (kDh - 1) : c % dhv;
-        return (e & 1) ? (partner * ax.sn + v * ax.cs) : (v * ax.cs - partner * ax.sn);
+        return (e & 1) ? rope_odd(partner, v, ax.cs, ax.sn) : rope_even(v, partner, ax.cs, ax.sn);
     }
     __device__ void store(const Row& ri, const Aux& ax, int m, int n, float v, float partner) const {
         const int dhv = head_dim();
@@ -94,7 +116,10 @@ struct EpiQkv {
     // there: q and K rows as 16-byte chunks (eight lanes per head row), V^T one
     // row (= cache slot) per lane, so a wavefront's store covers consecutive
     // slots of one dimension instead of 16 dimensions of 4 rows
-    static constexpr bool stores_tile(int bt) { return sizeof(T) == 2 && (bt == 64 || bt == 128); }
+    // (the wide kernel stages its 256 x 256 tile the same way: four heads)
+    static constexpr bool stores_tile(int bt) {
+        return sizeof(T) == 2 && (bt == 64 || bt == 128 || bt == 256);
+    }
     template <int BT>
     __device__ int tile_ld() const { return part == 2 ? BT + 2 : BT + 8; }   // odd dwords; 16-byte rows
     // element (rl, cl) of the tile (local row and column), global column n
@@ -102,7 +127,8 @@ struct EpiQkv {
                           float partner) const {
         tile[rl * ld + cl] = f32_to_f16_rne(value(ax, n, v, partner));
     }
-    template <int BT>
+    // a tile of TR rows and BT columns written by NT threads
+    template <int BT, int TR = BT, int NT = 256>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
         const int t = threadIdx.x, ld = tile_ld<BT>();
         const int c0 = n0 - part * d;   // first column of the tile in its part
@@ -110,8 +136,8 @@ struct EpiQkv {
         if (part < 2) {
             constexpr int kChunks = BT / 8;   // 16-byte chunks per row
 #pragma unroll
-            for (int h = 0; h < BT * kChunks / 256; ++h) {
-                const int qd = t + 256 * h, r = qd / kChunks, col = (qd % kChunks) * 8, m = m0 + r;
+            for (int h = 0; h < TR * kChunks / NT; ++h) {
+                const int qd = t + NT * h, r = qd / kChunks, col = (qd % kChunks) * 8, m = m0 + r;
                 if (m < M) {
                     const Row ri = row_info(m);
                     T* dst = part == 0 ? q + ri.off + c0 + col
@@ -121,8 +147,8 @@ struct EpiQkv {
                 }
             }
         } else {
-            constexpr int kGroups = 256 / BT;   // threads per row, each a strided set of columns
-            const int r = t % BT, m = m0 + r;
+            constexpr int kGroups = NT / TR;   // threads per row, each a strided set of columns
+            const int r = t % TR, m = m0 + r;
             if (m < M) {
                 const Row ri = row_info(m);
                 T* dst = kv + ri.off + head * 64 * 64;
@@ -130,6 +156,57 @@ struct EpiQkv {
                 for (int k = 0; k < BT / kGroups; ++k) {
                     const int e = t / BT + kGroups * k;
                     dst[(e >> 6) * 64 * 64 + (e & 63) * 64] = tile[r * ld + e];
+                }
+            }
+        }
+    }
+    // The wide kernel's path: RH rows of a BT-column tile staged in LDS as fp32
+    // sums before RoPE, tile[(r - rb) * ld + c] for tile rows rb .. rb + RH - 1,
+    // written by NT threads. q and K: each thread takes 8 consecutive columns
+    // (four pairs of one head) of a row, fetches their four cos and four sin
+    // values as two 16-byte loads, turns the pairs and stores 16 bytes. V^T:
+    // each thread a row (= cache slot) and a strided set of dimensions.
+    template <int BT, int RH, int NT>
+    __device__ void store_rows_f32(const float* tile, int ld, int n0, int m0, int rb, int M) const {
+        const int t = threadIdx.x;
+        const int c0 = n0 - part * d;
+        const int head = c0 >> 6;
+        if (part < 2) {
+            constexpr int kChunks = BT / 8;
+#pragma unroll
+            for (int h = 0; h < RH * kChunks / NT; ++h) {
+                const int qd = t + NT * h, r = qd / kChunks, col = (qd % kChunks) * 8;
+                const int m = m0 + rb + r;
+                if (m >= M) continue;
+                const Row ri = row_info(m);
+                const float4 xa = *reinterpret_cast<const float4*>(tile + r * ld + col);
+                const float4 xb = *reinterpret_cast<const float4*>(tile + r * ld + col + 4);
+                const int pi = ri.p * (kDh >> 1) + (((c0 + col) & (kDh - 1)) >> 1);
+                const float4 cs = *reinterpret_cast<const float4*>(rc + pi);
+                const float4 sn = *reinterpret_cast<const float4*>(rs + pi);
+                const float x[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+                const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
+                u32x4_t out;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t lo = f32_to_f16_rne(rope_even(x[2 * k], x[2 * k + 1], c4[k], s4[k]));
+                    const uint32_t hi = f32_to_f16_rne(rope_odd(x[2 * k], x[2 * k + 1], c4[k], s4[k]));
+                    out[k] = lo | (hi << 16);
+                }
+                T* dst = part == 0 ? q + ri.off + c0 + col
+                                   : kv + ri.off + (head + (col >> 6)) * 64 * 64 + (col & 63);
+                *reinterpret_cast<u32x4_t*>(dst) = out;
+            }
+        } else {
+            constexpr int kGroups = NT / RH;
+            const int r = t % RH, m = m0 + rb + r;
+            if (m < M) {
+                const Row ri = row_info(m);
+                T* dst = kv + ri.off + head * 64 * 64;
+#pragma unroll 8
+                for (int k = 0; k < BT / kGroups; ++k) {
+                    const int e = t / RH + kGroups * k;
+                    dst[(e >> 6) * 64 * 64 + (e & 63) * 64] = f32_to_f16_rne(tile[r * ld + e]);
                 }
             }
         }
@@ -178,23 +255,23 @@ struct EpiSwiGLU {
         Elem<T>::store(act + (size_t)m * ld + (n >> 1), swiglu(v, partner));
     }
     // fp16 square tiles of BT columns give BT rows of BT / 2 outputs, staged
-    // in LDS and written as 16-byte chunks per row. Only the 64x64 tile uses
-    // it: at 128x128 the staging measured slower than storing from registers
-    // (stress rounds 48 -> 53 us per launch)
-    static constexpr bool stores_tile(int bt) { return sizeof(T) == 2 && bt == 64; }
+    // in LDS and written as 16-byte chunks per row. The 64x64 tile and the
+    // wide kernel's 256x256 one use it: at 128x128 the staging measured slower
+    // than storing from registers (stress rounds 48 -> 53 us per launch)
+    static constexpr bool stores_tile(int bt) { return sizeof(T) == 2 && (bt == 64 || bt == 256); }
     template <int BT>
     __device__ int tile_ld() const { return BT / 2 + 8; }
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux&, int, float v,
                           float partner) const {
         if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_f16_rne(swiglu(v, partner));
     }
-    template <int BT>
+    template <int BT, int TR = BT, int NT = 256>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
         constexpr int kChunks = BT / 16;   // 16-byte chunks per row of BT / 2 outputs
         const int t = threadIdx.x, ldt = tile_ld<BT>();
 #pragma unroll
-        for (int h = 0; h < BT * kChunks / 256; ++h) {
-            const int qd = t + 256 * h, r = qd / kChunks, ch = qd % kChunks, m = m0 + r;
+        for (int h = 0; h < TR * kChunks / NT; ++h) {
+            const int qd = t + NT * h, r = qd / kChunks, ch = qd % kChunks, m = m0 + r;
             if (m < M)
                 *reinterpret_cast<u32x4_t*>(act + (size_t)m * ld + (n0 >> 1) + ch * 8) =
                     *reinterpret_cast<const u32x4_t*>(tile + r * ldt + ch * 8);
@@ -269,6 +346,13 @@ constexpr auto epi_stores_tile(int bt) -> decltype(E::stores_tile(0), bool()) {
 }
 template <typename E>
 constexpr bool epi_stores_tile(long) { return false; }
+// an epilogue may take the wide kernel's tile as fp32 rows (store_rows_f32)
+template <typename E>
+constexpr auto epi_stages_f32(int) -> decltype(&E::template store_rows_f32<256, 128, 512>, bool()) {
+    return true;
+}
+template <typename E>
+constexpr bool epi_stages_f32(long) { return false; }
 
 // one 16-byte chunk per lane from global memory to LDS: lane l's chunk lands
 // at lds + 16 l (lds is the same for the whole wavefront)
@@ -286,12 +370,26 @@ __device__ __forceinline__ void wait_loads() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
+// Which of a wide-tile launch and the 128 x 128 launch beside it does the
+// work, from the rows present (read on the device): rounds of tiles per CU
+// times a per-tile time fitted to measured launches (hundredths of a
+// microsecond per 64-deep step, plus a fixed part): 256 x 256 tiles one per
+// CU at 9 + 1.35 s us, 128 x 128 tiles two per CU at 17.4 + 0.6 s us. Both
+// kernels evaluate it in the same integer arithmetic, so exactly one works.
+__host__ __device__ inline bool wide_works(int M, int N, int K, int splits, int cus) {
+    const int s = K / splits / 64;
+    const long t256 = (long)((M + 255) / 256) * (N / 256) * splits;
+    const long t128 = (long)((M + 127) / 128) * (N / 128) * splits;
+    const long rw = (t256 + cus - 1) / cus, rf = (t128 + 2 * cus - 1) / (2 * cus);
+    return rw * (900 + 135 * s) <= rf * (1740 + 60 * s);
+}
+
 template <int BM, int BN, int WGM, int WGN, int NS, bool kDirect, typename Epi>
 __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A, int lda,
                                                   const uint16_t* __restrict__ W, float wscale,
                                                   int N, int K, const int* __restrict__ m_dev,
-                                                  int m_cap, int splits, float* __restrict__ part,
-                                                  Epi epi) {
+                                                  int m_cap, int splits, int pair_cus,
+                                                  float* __restrict__ part, Epi epi) {
     constexpr int BK = 64;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 16, TN = WN / 16;
@@ -301,22 +399,31 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
     __shared__ __attribute__((aligned(1024))) uint16_t S[(kDirect ? NS : 2) * STAGE];
 
     const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
-    const int tiles_m = (m_cap + BM - 1) / BM;
+    // launched beside the wide kernel (pair_cus = the CU count): the one of
+    // the two that wide_works picks does the work
+    if (pair_cus > 0 && wide_works(M, N, K, splits, pair_cus)) return;
+    if (M <= 0) return;
+    // Persistent: the grid holds about as many workgroups as the CUs keep
+    // resident, and each loops over tiles. The tiles of the rows present are
+    // numbered row tile fastest, then (column tile, split); XCD x (workgroups
+    // are dealt to the 8 XCDs round-robin) takes the x-th contiguous eighth,
+    // all row tiles of a few (column tile, split) pairs, so it reuses weight
+    // tiles in its own L2
+    const int tiles_m = (M + BM - 1) / BM;
     const int total = tiles_m * (N / BN) * splits;
     const int per_xcd = (total + 7) >> 3;
-    // workgroups are dealt to the 8 XCDs round-robin; each XCD gets a contiguous
-    // range of tiles (all M tiles of a few (N tile, split) pairs) so it reuses
-    // weight tiles in its own L2
-    const int lin = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
-    if (lin >= total) return;
+    const int xcd = (int)(blockIdx.x & 7);
+    const int lin_end = min((xcd + 1) * per_xcd, total);
+    const int Ks = K / splits;
+    const int nk = Ks / BK;
+    for (int lin = xcd * per_xcd + (int)(blockIdx.x >> 3); lin < lin_end;
+         lin += (int)(gridDim.x >> 3)) {
+    __syncthreads();   // the previous tile is done with LDS
     const int tm = lin % tiles_m;
     const int nz = lin / tiles_m;
     const int z = nz % splits, tn = nz / splits;
     const int m0 = tm * BM, n0 = tn * BN;
-    if (m0 >= M) return;
-    const int Ks = K / splits;
     const int kbase = z * Ks;
-    const int nk = Ks / BK;
 
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int wm = wv / WGN, wn = wv % WGN;
@@ -511,7 +618,7 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
 #pragma unroll
                 for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
             }
-        return;
+        continue;
     }
     if (!kPrefetchAux) {
 #pragma unroll
@@ -541,7 +648,7 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
             }
         __syncthreads();
         epi.template store_tile<BN>(tile, n0, m0, M);
-        return;
+        continue;
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -559,46 +666,334 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
                 if (ok) epi.store(rinfo[i][v], aux[i][v][j], row, col0 + j * 16, val, partner);
             }
         }
+    }
+}
+
+static int g_cus = 256;   // compute units of the device (gemm_setup)
+static int g_force_tile = 0;   // HBSJD_GEMM_TILE: 1 "wide", -1 "small", 0 chosen per launch
+
+// workgroups of a 256-thread kernel one CU holds at once (looked up once per
+// kernel; at least 1)
+static int resident(const void* kern) {
+    static std::mutex mu;
+    static std::map<const void*, int> seen;
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = seen.find(kern);
+    if (it != seen.end()) return it->second;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 256, 0) != hipSuccess || n < 1) n = 1;
+    seen[kern] = n;
+    return n;
+}
+
+// ---------------------------------------------------------------- wide tile
+// Launches with at least one 256 x 256 tile per CU take this kernel: 512
+// threads as 2 x 4 wavefronts, each a 128 x 64 block of 8 x 4
+// v_mfma_f32_16x16x32_f16 tiles whose 32 accumulators live in VGPRs (two
+// wavefronts per SIMD share the register file; a 128 x 128 block per
+// wavefront would fill all 256 AGPRs and the compiler then shuffles
+// accumulators through VGPRs every step, measured at 0.31 of the MFMA rate
+// against 0.47 for two 128 x 64 blocks). K advances 64 deep per step through
+// two 64 KB LDS stages filled straight from global memory (rows of eight
+// 16-byte chunks, chunk c of row r at c ^ (r & 7)): the loads of step k+1 are
+// issued when step k starts. Tiles are dealt so that each XCD's concurrent
+// workgroups cover about 4 row tiles x 8 column tiles, which its L2 serves
+// from one read of each operand slice. Split-K, wscale and the epilogues are those
+// of k_gemm_f16; staged epilogues stage the whole 256 x 256 tile in LDS.
+constexpr int kWideM = 256, kWideN = 256, kWideK = 64;
+constexpr int kWideStage = (kWideM + kWideN) * kWideK * 2;    // 64 KB
+constexpr int kWideLds = kWideM * (kWideN + 8) * 2;           // the staged tile (> 2 stages)
+static_assert(kWideLds >= 2 * kWideStage && kWideLds >= kWideM / 2 * (kWideN + 4) * 4,
+              "LDS of the wide kernel");
+
+template <typename Epi>
+__global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict__ A, int lda,
+                                                      const uint16_t* __restrict__ W, float wscale,
+                                                      int N, int K, const int* __restrict__ m_dev,
+                                                      int m_cap, int splits, int pair_cus,
+                                                      float* __restrict__ part, Epi epi) {
+    constexpr int TM = 8, TN = 4, WM = TM * 16, WN = TN * 16;
+    constexpr int LPW = (kWideM + kWideN) / 8 / 8;   // 16-byte loads per wavefront per stage
+    extern __shared__ __attribute__((aligned(1024))) uint16_t smem[];
+
+    // Persistent: the grid has at most one workgroup per CU (G of them, a
+    // multiple of 8, dealt to the XCDs round-robin) and each loops over
+    // tiles. The tiles of the rows present this launch (M <= m_cap) are
+    // numbered in groups of kGroup row tiles, column-major inside a group; XCD
+    // x takes the x-th contiguous eighth of that order and its G / 8
+    // workgroups stride through it, so the concurrent tiles of an XCD share
+    // operand slices in its L2 and every XCD gets an equal share however few
+    // rows are present. Launched beside k_gemm_f16 (pair_cus = the CU count),
+    // it works only when wide_works picks it.
+    const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
+    if (M <= 0) return;
+    const int tiles_m = (M + kWideM - 1) / kWideM, tiles_n = N / kWideN;
+    if (pair_cus > 0 && !wide_works(M, N, K, splits, pair_cus)) return;
+    const int total = tiles_m * tiles_n * splits;
+    const int per_xcd = (total + 7) >> 3;
+    const int xcd = (int)(blockIdx.x & 7), slot = (int)(blockIdx.x >> 3);
+    const int stride = (int)(gridDim.x >> 3);
+    const int lin_end = min((xcd + 1) * per_xcd, total);
+    const int Ks = K / splits;
+    const int nk = Ks / kWideK;
+    constexpr int kGroup = 4;
+
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int wm = wv >> 2, wn = wv & 3;
+    const int lr = lane >> 3, lp = lane & 7;
+    const int fr = lane & 15, fc = lane >> 4;
+    // fragment offsets (elements) of the two 32-deep halves of a stage
+    int aoff[2][TM], boff[2][TN];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int r = wm * WM + i * 16 + fr;
+            aoff[h][i] = r * kWideK + (((4 * h + fc) ^ (r & 7)) << 3);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int r = wn * WN + j * 16 + fr;
+            boff[h][j] = kWideM * kWideK + r * kWideK + (((4 * h + fc) ^ (r & 7)) << 3);
+        }
+    }
+
+    for (int lin = xcd * per_xcd + slot; lin < lin_end; lin += stride) {
+        const int z = lin % splits, tl = lin / splits;
+        const int grp = tl / (kGroup * tiles_n), first = grp * kGroup;
+        const int gsz = min(tiles_m - first, kGroup);
+        const int in = tl - grp * kGroup * tiles_n;
+        const int tm = first + in % gsz, tn = in / gsz;
+        const int m0 = tm * kWideM, n0 = tn * kWideN;
+        const int kbase = z * Ks;
+
+        // wavefront wv loads 8-row blocks wv, wv + 8, ... of A then of W
+        const uint16_t* src[LPW];
+#pragma unroll
+        for (int i = 0; i < LPW; ++i) {
+            const int f = wv + 8 * i;
+            const int r = 8 * (f < kWideM / 8 ? f : f - kWideM / 8) + lr;
+            const int c = (lp ^ (r & 7)) * 8;
+            src[i] = f < kWideM / 8 ? A + (size_t)min(m0 + r, M - 1) * lda + kbase + c
+                                    : W + (size_t)(n0 + r) * K + kbase + c;
+        }
+        auto issue = [&](int kt, int st) {
+            kt = kt < nk ? kt : nk - 1;
+            uint16_t* sb = smem + st * (kWideStage / 2);
+#pragma unroll
+            for (int i = 0; i < LPW; ++i) load_to_lds16(src[i] + kt * kWideK, sb + (wv + 8 * i) * 512);
+        };
+
+        f32x4_t acc[TM][TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+        __syncthreads();   // the previous tile's epilogue is done with LDS
+        issue(0, 0);
+        for (int kt = 0; kt < nk; ++kt) {
+            wait_loads<0>();
+            lds_barrier();
+            issue(kt + 1, (kt + 1) & 1);   // the last step re-reads its own tile into the idle stage
+            const uint16_t* sb = smem + (kt & 1) * (kWideStage / 2);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                f16x8_t a[TM], b[TN];
+#pragma unroll
+                for (int j = 0; j < TN; ++j) b[j] = *reinterpret_cast<const f16x8_t*>(sb + boff[h][j]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i) a[i] = *reinterpret_cast<const f16x8_t*>(sb + aoff[h][i]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j],
+                                                                            0, 0, 0);
+            }
+        }
+        wait_loads<0>();   // the last (redundant) stage load has landed before LDS is reused
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] *= wscale;
+
+        const int col0 = n0 + wn * WN + (lane & 15);
+        if (part) {
+            float* P = part + (size_t)z * m_cap * N;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+                    if (row >= M) continue;
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
+                }
+            continue;
+        }
+        Epi e = epi;
+        e.begin_tile(n0);
+        if constexpr (epi_stages_f32<Epi>(0)) {
+            // two passes of 128 rows (the wavefronts of one wm each) in fp32
+            constexpr int kLd = kWideN + 4;
+            float* ft = reinterpret_cast<float*>(smem);
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                __syncthreads();   // operand stages, or the previous pass, are done with LDS
+                if (wm == half) {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+#pragma unroll
+                            for (int j = 0; j < TN; ++j)
+                                ft[(i * 16 + 4 * (lane >> 4) + v) * kLd + wn * WN + j * 16 + (lane & 15)] =
+                                    acc[i][j][v];
+                }
+                __syncthreads();
+                e.template store_rows_f32<kWideN, kWideM / 2, 512>(ft, kLd, n0, m0, half * (kWideM / 2), M);
+            }
+            continue;
+        } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
+            __syncthreads();   // every wavefront is done with the operand stages
+            const int ld = e.template tile_ld<kWideN>();
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int rl = wm * WM + i * 16 + 4 * (lane >> 4) + v;
+                    const typename Epi::Row ri = e.row_info(min(m0 + rl, M - 1));
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const float val = acc[i][j][v];
+                        const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
+                            0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
+                        e.stage(smem, ld, rl, wn * WN + j * 16 + (lane & 15),
+                                e.aux(ri, col0 + j * 16), col0 + j * 16, val, partner);
+                    }
+                }
+            __syncthreads();
+            e.template store_tile<kWideN, kWideM, 512>(smem, n0, m0, M);
+            continue;
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+                const bool ok = row < M;
+                const typename Epi::Row ri = e.row_info(min(row, M - 1));
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const float val = acc[i][j][v];
+                    const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
+                        0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
+                    if (ok) e.store(ri, e.aux(ri, col0 + j * 16), row, col0 + j * 16, val, partner);
+                }
+            }
+    }
+}
+
+// the wide kernel needs more than 64 KB of dynamic LDS: allowed once per
+// epilogue type (at library set-up, before any graph capture)
+template <typename Epi>
+static hipError_t wide_allow_lds() {
+    return hipFuncSetAttribute((const void*)k_gemm_wide<Epi>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, kWideLds);
+}
+
+template <typename Epi>
+static void launch_wide(const void* A, int lda, const void* W, float wscale, int N, int K,
+                        const int* m_dev, int m_cap, int splits, int pair_cus, float* part,
+                        const Epi& epi, hipStream_t s) {
+    const int tiles = ((m_cap + kWideM - 1) / kWideM) * (N / kWideN) * splits;
+    const int cap = (g_cus / 8) * 8;
+    const int grid = std::max(8, std::min(cap, ((tiles + 7) / 8) * 8));
+    launch(k_gemm_wide<Epi>, dim3(grid), dim3(512), (uint32_t)kWideLds, s, (const uint16_t*)A, lda,
+           (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits, pair_cus, part, epi);
 }
 
 template <int BM, int BN, int WGM, int WGN, typename Epi>
 static void launch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
                        const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
-                       hipStream_t s) {
+                       hipStream_t s, int pair_cus = 0) {
     if (m_cap <= 0) return;
     const int tiles = ((m_cap + BM - 1) / BM) * (N / BN) * splits;
-    const int grid = ((tiles + 7) / 8) * 8;
+    // persistent grid: as many workgroups as the CUs hold at once
+    auto grid_for = [&](const void* kern) {
+        return std::min(((tiles + 7) / 8) * 8, std::max(8, (g_cus * resident(kern) / 8) * 8));
+    };
     if constexpr (BM * BN >= 128 * 128) {
         // the large tiles have enough MFMA work per step to cover a shallow
         // register pipeline (direct staging measured no faster there)
+        const int grid = grid_for((const void*)k_gemm_f16<BM, BN, WGM, WGN, 3, false, Epi>);
         launch(k_gemm_f16<BM, BN, WGM, WGN, 3, false, Epi>, dim3(grid), dim3(256), 0, s,
                (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
-               part, epi);
+               pair_cus, part, epi);
     } else if (tiles <= 512) {
         // direct staging, 4 stages (64 KB of LDS): two workgroups per CU hold
         // the whole launch
+        const int grid = grid_for((const void*)k_gemm_f16<BM, BN, WGM, WGN, 4, true, Epi>);
         launch(k_gemm_f16<BM, BN, WGM, WGN, 4, true, Epi>, dim3(grid), dim3(256), 0, s,
                (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
-               part, epi);
+               pair_cus, part, epi);
     } else {
         // more tiles than two per CU: 3 stages (48 KB), three workgroups per CU
+        const int grid = grid_for((const void*)k_gemm_f16<BM, BN, WGM, WGN, 3, true, Epi>);
         launch(k_gemm_f16<BM, BN, WGM, WGN, 3, true, Epi>, dim3(grid), dim3(256), 0, s,
                (const uint16_t*)A, lda, (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits,
-               part, epi);
+               pair_cus, part, epi);
     }
 }
 
 // tile choice by the launch's row cap (the same for Full and Compact rounds):
 // large tiles once there are enough of them to fill the 256 CUs twice over
+// Launches whose rows are only known on the device (m_dev) and that could
+// fill the wide kernel take both it and the smaller-tile kernel; each reads
+// the row count and wide_works tells which one works. (A persistent launch
+// that finds no work costs a few microseconds; a wide-tile launch sized for
+// the capacity would cost its idle workgroups' dispatch, about as much as
+// the work of a full launch.)
+constexpr int kWideMin = 96;   // capacity in 256 x 256 tiles below which it is not tried
+
 template <typename Epi>
 static void dispatch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
                          const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
-                         hipStream_t s) {
+                         hipStream_t s, bool wide_ok = true) {
+    const long t256 = (long)((m_cap + 255) / 256) * (N / 256) * splits;
     const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
+    const bool fit = wide_ok && N % 256 == 0 && (K / splits) % kWideK == 0;
+    if (g_force_tile != 0) {   // HBSJD_GEMM_TILE: one kernel for every launch (results are the same)
+        if (g_force_tile > 0 && fit) {
+            launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
+        } else if (N % 128 == 0 && t128 >= 512) {
+            launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        } else {
+            launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        }
+        return;
+    }
+    const bool wide = fit && t256 >= kWideMin;
+    if (wide && !m_dev) {   // the rows are known here: the same choice on the host
+        if (wide_works(m_cap, N, K, splits, g_cus)) {
+            launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
+            return;
+        }
+    }
+    if (!m_dev) {
+        if (N % 128 == 0 && t128 >= 512)
+            launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        else
+            launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        return;
+    }
+    const int pair = wide ? g_cus : 0;
+    if (wide) launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, pair, part, epi, s);
     if (N % 128 == 0 && t128 >= 512)
-        launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
     else
-        launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
+        launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
 }
 
 // ---------------------------------------------------------------- fp32
@@ -681,7 +1076,8 @@ void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int
     if (f16) {
         EpiQkv<uint16_t> epi{(uint16_t*)e.q, (uint16_t*)e.kv, e.pos, e.kvslot, e.rope_cos,
                              e.rope_sin, e.d, e.heads, e.head_dim, e.T};
-        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s);
+        // a 256-column tile must lie inside one of q, k and v
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, epi, s, e.d % 256 == 0);
     } else {
         EpiQkv<float> epi{(float*)e.q, (float*)e.kv, e.pos, e.kvslot, e.rope_cos, e.rope_sin,
                           e.d, e.heads, e.head_dim, e.T};
@@ -692,21 +1088,24 @@ void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int
 template <int Tag>   // 0 the O projection, 1 W2 (distinct kernel names in traces)
 struct PartialTag {};
 
+// the split-K partial sums are written by the kernel itself; no epilogue
+template <int Tag>
+struct EpiNone {
+    struct Row {};
+    struct Aux {};
+    __device__ void begin_tile(int) {}
+    __device__ Row row_info(int) const { return Row{}; }
+    __device__ Aux aux(const Row&, int) const { return Aux{}; }
+    __device__ void store(const Row&, const Aux&, int, int, float, float) const {}
+    PartialTag<Tag> tag;
+};
+
 template <int Tag>
 static void partial_tag(bool f16, const void* A, int lda, const void* W, float wscale, int N,
                         int K, const int* m_dev, int m_cap, int splits, float* part,
                         hipStream_t s) {
     if (f16) {
-        struct EpiNone {
-            struct Row {};
-            struct Aux {};
-            __device__ void begin_tile(int) {}
-            __device__ Row row_info(int) const { return Row{}; }
-            __device__ Aux aux(const Row&, int) const { return Aux{}; }
-            __device__ void store(const Row&, const Aux&, int, int, float, float) const {}
-            PartialTag<Tag> tag;
-        };
-        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, EpiNone{}, s);
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, EpiNone<Tag>{}, s);
     } else {
         launch_f32(A, lda, W, N, K, m_dev, m_cap, EpiStore{part, N}, s);
     }
@@ -746,6 +1145,25 @@ void gemm_logits(bool f16, const void* A, int lda, const void* W, float wscale, 
         else
             launch_f32(A, lda, W, N, K, m_dev, m_cap, epi, s);
     }
+}
+
+static_assert(epi_stages_f32<EpiQkv<uint16_t>>(0) && !epi_stages_f32<EpiSwiGLU<uint16_t>>(0),
+              "the wide kernel stages QKV tiles as fp32 rows");
+
+hipError_t gemm_setup() {
+    const char* f = std::getenv("HBSJD_GEMM_TILE");
+    g_force_tile = !f ? 0 : std::strcmp(f, "wide") == 0 ? 1 : std::strcmp(f, "small") == 0 ? -1 : 0;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus >= 8)
+        g_cus = cus;
+    const hipError_t e[] = {wide_allow_lds<EpiQkv<uint16_t>>(), wide_allow_lds<EpiSwiGLU<uint16_t>>(),
+                            wide_allow_lds<EpiLogits<true>>(), wide_allow_lds<EpiLogits<false>>(),
+                            wide_allow_lds<EpiNone<0>>(), wide_allow_lds<EpiNone<1>>()};
+    for (hipError_t x : e)
+        if (x != hipSuccess) return x;
+    return hipSuccess;
 }
 
 }  // namespace hbsjd

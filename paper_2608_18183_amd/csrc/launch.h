@@ -10,9 +10,11 @@
 
 namespace hbsjd {
 
-// Optional kernel timing: when a caller arms the per-thread slot, the next
-// launch through launch() carries the start/stop events in its own dispatch
-// (hipExtLaunchKernelGGL), so they time the kernel itself.
+// Optional kernel timing: while a caller has the per-thread slot armed, the
+// launches through launch() carry the events in their own dispatches
+// (hipExtLaunchKernelGGL): the first one the start event, every one the stop
+// event, so the pair spans the kernels of the armed region (one GEMM may be
+// two launches, of which one finds nothing to do) and nothing else.
 struct LaunchEvents {
     hipEvent_t start = nullptr;
     hipEvent_t stop = nullptr;
@@ -23,9 +25,10 @@ LaunchEvents* launch_events();
 template <typename K, typename... Args>
 inline void launch(K kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
     LaunchEvents* ev = launch_events();
-    if (ev->start && !ev->used) {
+    if (ev->start) {
+        hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev->used ? nullptr : ev->start,
+                              ev->stop, 0u, args...);
         ev->used = true;
-        hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev->start, ev->stop, 0u, args...);
     } else {
         hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
     }
@@ -76,6 +79,8 @@ struct QkvArgs {
 // ignores wscale.
 void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
               const int* m_dev, int m_cap, const QkvArgs& e, hipStream_t s);
+// once per process before any launch (the wide GEMM's LDS allowance)
+hipError_t gemm_setup();
 // split-K partial sums part[split][m_cap][N] (tag 0: O projection, 1: W2);
 // split_for() is the split count the host must size `part` for
 int split_for(int m_cap, int N, int K);

@@ -638,3 +638,38 @@ def test_profile_sampling_brackets_one_launch_in_every(tiny):
         with pytest.raises(P().HbsjdError) as ei:
             ctx.hbsjd_profile_sample(bad)
         assert ei.value.code == "EINVAL"
+
+
+# ------------------------------------------------------------------ GEMM kernel choice
+
+
+@pytest.mark.parametrize("name", ["stress_b", "llamagen_xl_cfg"])
+def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
+    """Every projection may run on the wide 256 x 256 kernel or on the 128 x 128
+    / 64 x 64 one, chosen per launch from the rows present; Full and Compact
+    rounds (Sec. 4.3) process the same row in launches of different sizes, so
+    the kernels must agree bit for bit. Forward logits of the same sequences
+    with every launch forced onto one kernel (HBSJD_GEMM_TILE) and chosen per
+    launch must be identical, at a row count where the choice varies."""
+    wl = synth.WORKLOADS[name]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0, std=wl.weight_std, bias_std=wl.bias_std)
+    rng = np.random.default_rng(5)
+    n = 12 if shape.T > 300 else 24
+    lens = np.full(n, shape.T - 1, dtype=np.int32)
+    lens[1] = 17
+    toks = rng.integers(0, shape.vocab, size=(n, shape.T)).astype(np.int32)
+    labels = rng.integers(0, shape.n_classes + 1, size=n).astype(np.int32)
+    outs = {}
+    for force in ["wide", "small", ""]:
+        if force:
+            monkeypatch.setenv("HBSJD_GEMM_TILE", force)
+        else:
+            monkeypatch.delenv("HBSJD_GEMM_TILE", raising=False)
+        ctx = gu.make_ctx(shape, "bf16", blob)
+        outs[force] = ctx.hbsjd_forward(torch.from_numpy(toks).cuda(), lens.tolist(),
+                                        labels).cpu().numpy()
+        del ctx
+    monkeypatch.delenv("HBSJD_GEMM_TILE", raising=False)
+    assert np.array_equal(outs["wide"].view(np.uint32), outs["small"].view(np.uint32))
+    assert np.array_equal(outs[""].view(np.uint32), outs["small"].view(np.uint32))
