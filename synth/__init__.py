@@ -151,13 +151,21 @@ def bf16_rounded_blob(m: ModelShape, blob: np.ndarray) -> np.ndarray:
     it is given the same way) and the fp32 oracle of a bf16 comparison see
     these values."""
     out = np.array(blob, dtype=np.float32, copy=True)
+    chunk = 1 << 20                  # in place, a cache-sized piece at a time
+    t = np.empty(chunk, dtype=np.uint32)
     off = 0
     for _, shape, kind in blob_layout(m):
         k = int(np.prod(shape))
         if kind == "w":
             u = out[off:off + k].view(np.uint32)
-            u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
-            u &= np.uint32(0xFFFF0000)
+            for s in range(0, k, chunk):
+                v = u[s:s + chunk]
+                r = t[:v.size]
+                np.right_shift(v, np.uint32(16), out=r)
+                np.bitwise_and(r, np.uint32(1), out=r)
+                np.add(r, np.uint32(0x7FFF), out=r)
+                np.add(v, r, out=v)
+                np.bitwise_and(v, np.uint32(0xFFFF0000), out=v)
         off += k
     return out
 

@@ -44,10 +44,112 @@ def test_rollout_work_gemm_launches_by_hand():
     k = np.array([100, 255], dtype=np.int32)
     counts = np.array([[5, 1], [4, 0], [0, 0]], dtype=np.int32)
     d, L = 768, 12
-    b, fl = bench.rollout_work("qkv", shape, k, counts, 16, 1)
-    per = lambda rows: (3 * d * d * 2 + rows * d * 2 + rows * 3 * d * 2, 2.0 * rows * 3 * d * d)
+    alg, act, fl, n = bench.rollout_work("qkv", shape, k, counts, 16, 1)
+    # algorithmic: the weights and the K, V rows appended to the cache;
+    # activations: the normed input rows and the q rows
+    per = lambda rows: (3 * d * d * 2 + rows * 2 * d * 2, rows * d * 2 + rows * d * 2,
+                        2.0 * rows * 3 * d * d)
     # prefill, then rounds with 2, 1 and 1 active images (image 0 is still
     # short of T after the last listed round)
     rows = [101 + 256, 2 * 17, 1 * 17, 1 * 17]
-    assert b == sum(L * per(r)[0] for r in rows)
-    assert fl == sum(L * per(r)[1] for r in rows)
+    assert alg == sum(L * per(r)[0] for r in rows)
+    assert act == sum(L * per(r)[1] for r in rows)
+    assert fl == sum(L * per(r)[2] for r in rows)
+    assert n == 4 * L
+
+
+def test_rollout_work_attention_and_lm_head_by_hand():
+    """Attention reads each sequence's committed K and V once per layer (the
+    whole prefix in the prefill) and attends (W + 1)(n + 1) + W(W + 1)/2 keys
+    per round and sequence; the lm_head reads its weights and writes one fp32
+    logits row per row, on the last prefill row of each sequence only. Two
+    guidance branches double every row."""
+    shape = synth.small_shape(n_layers=2, d_model=64, n_heads=1, mlp_hidden=128, vocab=256,
+                              n_classes=3, grid=4)          # T = 16
+    d, V, L, W = 64, 256, 2, 4
+    k = np.array([5, 16], dtype=np.int32)                  # image 1 is complete
+    counts = np.array([[3, 0], [0, 0]], dtype=np.int32)    # 5 -> 8 -> 8
+    for cfg in (1, 2):
+        alg, act, fl, n = bench.rollout_work("attn", shape, k, counts, W, cfg)
+        keys_pf = sum(range(1, 7))                          # rows 0..5 attend 1..6 keys
+        keys_r = [5 * (c + 1) + W * (W + 1) // 2 for c in (5, 8)]
+        assert fl == 4.0 * d * L * cfg * (keys_pf + sum(keys_r))
+        assert alg == L * cfg * 2 * d * 2 * (6 + 5 + 8)
+        assert act == L * cfg * 2 * d * 2 * (6 + 5 + 5)
+        assert n == 3 * L
+        alg, act, fl, n = bench.rollout_work("lmhead", shape, k, counts, W, cfg)
+        rows = cfg * (1 + 5 + 5)
+        assert alg == 3 * d * V * 2 + rows * V * 4
+        assert act == rows * d * 2
+        assert fl == 2.0 * rows * d * V and n == 3
+
+
+# ------------------------------------------------------------------ rocprofv3 summaries
+
+_WIDE = "void hbsjd::k_gemm_wide<hbsjd::EpiSwiGLU<unsigned short> >(unsigned short const*, int)"
+_SMALL = ("void hbsjd::k_gemm_f16<128, 128, 2, 2, 3, false, hbsjd::EpiSwiGLU<unsigned short> >"
+          "(unsigned short const*, int)")
+_W2 = "void hbsjd::k_gemm_f16<64, 64, 2, 2, 3, true, hbsjd::EpiNone<1> >(unsigned short const*)"
+_ATTN = "void hbsjd::k_attn_f16<2>(unsigned short const*, unsigned short*, int)"
+
+
+def test_kernel_class_names():
+    assert bench.kernel_class(_WIDE) == ("w13", True)
+    assert bench.kernel_class(_SMALL) == ("w13", False)
+    assert bench.kernel_class(_W2) == ("w2", False)
+    assert bench.kernel_class(_ATTN) == ("attn", False)
+    assert bench.kernel_class("hbsjd::k_transform(hbsjd::TransformArgs)") == ("transform", False)
+    assert bench.kernel_class("hbsjd::k_transform_rows_setup(int)")[0] is None
+    assert bench.kernel_class("__amd_rocclr_copyBuffer")[0] is None
+
+
+def test_logical_launches_pair_wide_and_small_tile_dispatches():
+    """A wide dispatch followed at once by the smaller-tile kernel of the same
+    class is one launch; a small-tile dispatch alone (rows known on the host)
+    or after another class is a launch of its own."""
+    seq = [(1, _WIDE), (2, _SMALL), (3, _W2), (4, _SMALL), (5, _WIDE), (6, _ATTN),
+           (7, _SMALL), (8, _WIDE), (9, "__amd_rocclr_copyBuffer"), (10, _SMALL)]
+    groups = bench.logical_launches([{"id": i, "name": n} for i, n in reversed(seq)])
+    got = [(c, [d["id"] for d in ds]) for c, ds in groups]
+    assert got == [("w13", [1, 2]), ("w2", [3]), ("w13", [4]), ("w13", [5]), ("attn", [6]),
+                   ("w13", [7]), ("w13", [8]), ("w13", [10])]
+
+
+def _write_counters(path, rows):
+    import csv
+    import os
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "run_counter_collection.csv"), "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for r in rows:
+            w.writerow(r)
+
+
+def test_traffic_summary_scales_by_the_copy_and_sums_paired_dispatches(tmp_path):
+    """Counters in KiB summed over instances and over the two dispatches of a
+    paired launch, averaged over launches, divided by the copy's reading per
+    byte: FETCH_SIZE reads half of a 1 GiB copy (factor 0.5), WRITE_SIZE all."""
+    import json
+    gib_kib = (1 << 30) / 1024
+    _write_counters(tmp_path / "copy_FETCH_SIZE", [(7, "copy", "FETCH_SIZE", gib_kib / 4)] * 2)
+    _write_counters(tmp_path / "copy_WRITE_SIZE", [(7, "copy", "WRITE_SIZE", gib_kib / 2)] * 2)
+    # two w13 launches: (wide 100 + small 4) and (small 96) KiB fetched;
+    # instance rows of one dispatch add up
+    _write_counters(tmp_path / "bench_FETCH_SIZE",
+                    [(1, _WIDE, "FETCH_SIZE", 60), (1, _WIDE, "FETCH_SIZE", 40),
+                     (2, _SMALL, "FETCH_SIZE", 4), (3, _ATTN, "FETCH_SIZE", 10),
+                     (4, _SMALL, "FETCH_SIZE", 96)])
+    _write_counters(tmp_path / "bench_WRITE_SIZE",
+                    [(1, _WIDE, "WRITE_SIZE", 30), (2, _SMALL, "WRITE_SIZE", 2),
+                     (3, _ATTN, "WRITE_SIZE", 5), (4, _SMALL, "WRITE_SIZE", 32)])
+    out = tmp_path / "traffic.json"
+    out.write_text(json.dumps({"other": {"x": 1}}))
+    assert bench.traffic_summary(str(tmp_path), "wl", str(out)) == 0
+    rec = json.loads(out.read_text())
+    assert rec["other"] == {"x": 1}
+    w13 = rec["wl"]["w13"]
+    assert w13["launches"] == 2 and w13["copy_fetch_factor"] == 0.5
+    assert w13["fetch_kib_per_launch"] == 100.0 and w13["write_kib_per_launch"] == 32.0
+    assert w13["hbm_bytes_per_launch"] == int(100 * 1024 / 0.5 + 32 * 1024)
+    assert rec["wl"]["attn"]["hbm_bytes_per_launch"] == int(10 * 1024 / 0.5 + 5 * 1024)
