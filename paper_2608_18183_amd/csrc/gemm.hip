@@ -35,6 +35,11 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 // becomes a memcpy that keeps the stage arrays out of registers)
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
+// the value lane l ^ 1 holds (DPP quad permutation [1, 0, 3, 2])
+__device__ __forceinline__ float swap_lane_pair(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
 // ---------------------------------------------------------------- epilogues
 // operator()(row, col, value, value of column col ^ 1 in the same row)
 
@@ -246,9 +251,15 @@ struct EpiSwiGLU {
     __device__ void begin_tile(int) {}
     __device__ Row row_info(int) const { return Row{}; }
     __device__ Aux aux(const Row&, int) const { return Aux{}; }
-    // columns 2i / 2i+1 are the gate (W1 row i) and the up projection (W3 row i)
+    // columns 2i / 2i+1 are the gate (W1 row i) and the up projection (W3 row i).
+    // With an fp16 output the logistic's reciprocal is the hardware one (1 ulp
+    // in fp32, far below the output's rounding); fp32 outputs divide.
     __device__ static float swiglu(float gate, float up) {
-        return gate / (1.0f + __expf(-gate)) * up;
+        if constexpr (sizeof(T) == 2) {
+            return gate * __builtin_amdgcn_rcpf(1.0f + __expf(-gate)) * up;
+        } else {
+            return gate / (1.0f + __expf(-gate)) * up;
+        }
     }
     __device__ void store(const Row&, const Aux&, int m, int n, float v, float partner) const {
         if (n & 1) return;
@@ -264,6 +275,32 @@ struct EpiSwiGLU {
     __device__ void stage(uint16_t* tile, int ld, int rl, int cl, const Aux&, int, float v,
                           float partner) const {
         if (!(cl & 1)) tile[rl * ld + (cl >> 1)] = f32_to_f16_rne(swiglu(v, partner));
+    }
+    // Four rows rl0 .. rl0 + 3 of column cl at once, the layout of one MFMA
+    // accumulator: the lane holding the up column (odd cl) and its neighbour
+    // holding the gate column trade two values each, so the gate lane computes
+    // rows 0-1 and the up lane rows 2-3 and no lane computes a product it
+    // throws away.
+    __device__ void stage_quad(uint16_t* tile, int ld, int rl0, int cl, const f32x4_t& v) const {
+        const bool up_lane = cl & 1;
+        const float r0 = swap_lane_pair(up_lane ? v[0] : v[2]);
+        const float r1 = swap_lane_pair(up_lane ? v[1] : v[3]);
+        const float g0 = up_lane ? r0 : v[0], g1 = up_lane ? r1 : v[1];
+        const float u0 = up_lane ? v[2] : r0, u1 = up_lane ? v[3] : r1;
+        uint16_t* dst = tile + (rl0 + (up_lane ? 2 : 0)) * ld + (cl >> 1);
+        dst[0] = f32_to_f16_rne(swiglu(g0, u0));
+        dst[ld] = f32_to_f16_rne(swiglu(g1, u1));
+    }
+    // the same straight to the output rows m0 .. m0 + 3 (rows >= M skipped)
+    __device__ void store_quad(int m0, int n, const f32x4_t& v, int M) const {
+        const bool up_lane = n & 1;
+        const float r0 = swap_lane_pair(up_lane ? v[0] : v[2]);
+        const float r1 = swap_lane_pair(up_lane ? v[1] : v[3]);
+        const float g0 = up_lane ? r0 : v[0], g1 = up_lane ? r1 : v[1];
+        const float u0 = up_lane ? v[2] : r0, u1 = up_lane ? v[3] : r1;
+        const int m = m0 + (up_lane ? 2 : 0);
+        if (m < M) Elem<T>::store(act + (size_t)m * ld + (n >> 1), swiglu(g0, u0));
+        if (m + 1 < M) Elem<T>::store(act + (size_t)(m + 1) * ld + (n >> 1), swiglu(g1, u1));
     }
     template <int BT, int TR = BT, int NT = 256>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
@@ -346,6 +383,16 @@ constexpr auto epi_stores_tile(int bt) -> decltype(E::stores_tile(0), bool()) {
 }
 template <typename E>
 constexpr bool epi_stores_tile(long) { return false; }
+// an epilogue may stage the four rows of one MFMA accumulator at once (stage_quad)
+template <typename E>
+constexpr auto epi_stages_quads(int) -> decltype(&E::stage_quad, bool()) { return true; }
+template <typename E>
+constexpr bool epi_stages_quads(long) { return false; }
+// or store them from registers (store_quad)
+template <typename E>
+constexpr auto epi_stores_quads(int) -> decltype(&E::store_quad, bool()) { return true; }
+template <typename E>
+constexpr bool epi_stores_quads(long) { return false; }
 // an epilogue may take the wide kernel's tile as fp32 rows (store_rows_f32)
 template <typename E>
 constexpr auto epi_stages_f32(int) -> decltype(&E::template store_rows_f32<256, 128, 512>, bool()) {
@@ -632,6 +679,14 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
         __syncthreads();   // every wavefront is done with the operand stages
         uint16_t* tile = S;
         const int ld = epi.template tile_ld<BN>();
+        if constexpr (epi_stages_quads<Epi>(0)) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    epi.stage_quad(tile, ld, wm * WM + i * 16 + 4 * (lane >> 4),
+                                   wn * WN + j * 16 + (lane & 15), acc[i][j]);
+        } else {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -646,8 +701,17 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
                               col0 + j * 16, val, partner);
                 }
             }
+        }
         __syncthreads();
         epi.template store_tile<BN>(tile, n0, m0, M);
+        continue;
+    }
+    if constexpr (epi_stores_quads<Epi>(0)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                epi.store_quad(m0 + wm * WM + i * 16 + 4 * (lane >> 4), col0 + j * 16, acc[i][j], M);
         continue;
     }
 #pragma unroll
@@ -858,6 +922,14 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
         } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
             __syncthreads();   // every wavefront is done with the operand stages
             const int ld = e.template tile_ld<kWideN>();
+            if constexpr (epi_stages_quads<Epi>(0)) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        e.stage_quad(smem, ld, wm * WM + i * 16 + 4 * (lane >> 4),
+                                     wn * WN + j * 16 + (lane & 15), acc[i][j]);
+            } else {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -873,6 +945,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
                                 e.aux(ri, col0 + j * 16), col0 + j * 16, val, partner);
                     }
                 }
+            }
             __syncthreads();
             e.template store_tile<kWideN, kWideM, 512>(smem, n0, m0, M);
             continue;
