@@ -212,6 +212,171 @@ __global__ __launch_bounds__(256) void k_attn_f16(const uint16_t* __restrict__ q
     }
 }
 
+// fp16, one wavefront per (segment, query block, head) when a launch has
+// enough of them to fill the chip: the wavefront walks its keys' 64-key tiles
+// in order with one online softmax, the K and V fragments of tile t + 1 in
+// flight while tile t is multiplied, and needs no LDS and no merge. The score
+// and probability layouts are those of k_attn_f16 (S^T = K Q^T, O^T = V^T P^T).
+// A row's result depends only on its position and the cache contents.
+template <int NMT>
+__global__ __launch_bounds__(64) void k_attn_f16_seq(const uint16_t* __restrict__ qb,
+                                                     uint16_t* __restrict__ ob, int d, int H,
+                                                     const uint16_t* __restrict__ kv, int maxp,
+                                                     Segments seg, const int* __restrict__ nseg_dev,
+                                                     int qblocks) {
+    constexpr int QR = NMT * 16;
+    const int sb = blockIdx.x, head = blockIdx.y;
+    const int sg = sb / qblocks, qblk = sb - sg * qblocks;
+    const int lane = threadIdx.x;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int nseg = *nseg_dev;
+    const int nrows = seg.nrows[sg];
+    const int row0s = seg.row0[sg];
+    const int pos0 = seg.pos0[sg];
+    // the segment's page list, one entry per lane (maxp <= 64)
+    const int pagev = seg.pages[(size_t)sg * maxp + min(lane, maxp - 1)];
+    if (sg >= nseg) return;
+    const int q0 = qblk * QR;
+    if (q0 >= nrows) return;
+    const int nq = min(QR, nrows - q0);
+    const int row0 = row0s + q0;
+    const int posf = pos0 + q0;
+    const int ntiles = (posf + nq - 1) / 64 + 1;
+
+    f16x8_t qf[NMT][2];
+#pragma unroll
+    for (int i = 0; i < NMT; ++i) {
+        const int r = i * 16 + c16;
+        const int rr = min(r, nq - 1);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const f16x8_t x = load_f16x8(qb + (size_t)(row0 + rr) * d + head * 64 + kk * 32 + 8 * g);
+            qf[i][kk] = r < nq ? x : f16x8_t{};
+        }
+    }
+    f32x4_t o[NMT][4];
+    float m[NMT], l[NMT];
+#pragma unroll
+    for (int i = 0; i < NMT; ++i) {
+        m[i] = -INFINITY;
+        l[i] = 0.f;
+#pragma unroll
+        for (int dj = 0; dj < 4; ++dj) o[i][dj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    const int krow = 8 * (c16 >> 2) + (c16 & 3);
+    const size_t page_elems = (size_t)2 * H * 64 * 64;
+    // K and V fragments of one tile (the page of tile t is lane t's entry)
+    auto fetch = [&](int tile, f16x8_t (&kf)[4][2], f16x8_t (&vf)[4][2]) {
+        const int page = __builtin_amdgcn_readlane(pagev, tile);
+        const uint16_t* Kb = kv + (size_t)page * page_elems + (size_t)head * 4096;
+        const uint16_t* Vb = kv + (size_t)page * page_elems + (size_t)(H + head) * 4096;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int kd = 0; kd < 2; ++kd) {
+                kf[j][kd] = load_f16x8(Kb + (32 * (j >> 1) + 4 * (j & 1) + krow) * 64 + kd * 32 + 8 * g);
+                vf[j][kd] = load_f16x8(Vb + (j * 16 + c16) * 64 + kd * 32 + 8 * g);
+            }
+    };
+    // scores in log2 units: y = (q . k) / 8 * log2(e), p = 2^(y - max); rows
+    // past the segment (q = 0) are computed and never stored
+    constexpr float kScale = 0.125f * 1.44269504088896340736f;
+    auto tile_step = [&](int tile, const f16x8_t (&kf)[4][2], const f16x8_t (&vf)[4][2]) {
+        f32x4_t s[NMT][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int i = 0; i < NMT; ++i) s[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kd = 0; kd < 2; ++kd)
+#pragma unroll
+                for (int i = 0; i < NMT; ++i)
+                    s[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[j][kd], qf[i][kd], s[i][j],
+                                                                      0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < NMT; ++i) {
+            // element v of group j is key tile * 64 + 32 (j >> 1) + 8 g + 4 (j & 1) + v,
+            // visible while v <= lim - 32 (j >> 1) - 4 (j & 1)
+            const int lim = posf + i * 16 + c16 - tile * 64 - 8 * g;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float x = s[i][j][v] * kScale;
+                    if (v > lim - 32 * (j >> 1) - 4 * (j & 1)) x = -INFINITY;
+                    s[i][j][v] = x;
+                    mx = fmaxf(mx, x);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            // tile 0 holds key 0, which every row sees: the maximum is finite
+            // from the first tile on
+            const float mnew = fmaxf(m[i], mx);
+            const float alpha = exp2f(m[i] - mnew);
+            float ps = 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float pv = exp2f(s[i][j][v] - mnew);
+                    s[i][j][v] = pv;
+                    ps += pv;
+                }
+            l[i] = l[i] * alpha + ps;
+            m[i] = mnew;
+#pragma unroll
+            for (int dj = 0; dj < 4; ++dj) o[i][dj] *= alpha;
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int i = 0; i < NMT; ++i) {
+                f16x8_t pf;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    pf[e] = (_Float16)s[i][2 * kk][e];
+                    pf[4 + e] = (_Float16)s[i][2 * kk + 1][e];
+                }
+#pragma unroll
+                for (int dj = 0; dj < 4; ++dj)
+                    o[i][dj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf[dj][kk], pf, o[i][dj],
+                                                                       0, 0, 0);
+            }
+    };
+    // two register buffers; every fetch is issued (the last tile re-fetched
+    // past the end), so the loads in flight are the same on every path
+    f16x8_t ka[4][2], va[4][2], kb[4][2], vb[4][2];
+    fetch(0, ka, va);
+    for (int tile = 0; tile < ntiles; tile += 2) {
+        fetch(min(tile + 1, ntiles - 1), kb, vb);
+        tile_step(tile, ka, va);
+        if (tile + 1 >= ntiles) break;
+        fetch(min(tile + 2, ntiles - 1), ka, va);
+        tile_step(tile + 1, kb, vb);
+    }
+#pragma unroll
+    for (int i = 0; i < NMT; ++i) {
+        l[i] += __shfl_xor(l[i], 16, 64);
+        l[i] += __shfl_xor(l[i], 32, 64);
+    }
+    // lane (g, c16) holds dims dj * 16 + 4 g .. + 3 of query c16 + 16 i: four
+    // halves per store
+#pragma unroll
+    for (int i = 0; i < NMT; ++i) {
+        const int qr = i * 16 + c16;
+        if (qr >= nq) continue;
+        uint16_t* dst = ob + (size_t)(row0 + qr) * d + head * 64 + 4 * g;
+#pragma unroll
+        for (int dj = 0; dj < 4; ++dj) {
+            uint32_t w0 = f32_to_f16_rne(o[i][dj][0] / l[i]) | ((uint32_t)f32_to_f16_rne(o[i][dj][1] / l[i]) << 16);
+            uint32_t w1 = f32_to_f16_rne(o[i][dj][2] / l[i]) | ((uint32_t)f32_to_f16_rne(o[i][dj][3] / l[i]) << 16);
+            *reinterpret_cast<uint2*>(dst + dj * 16) = make_uint2(w0, w1);
+        }
+    }
+}
+
 // fp32: one wavefront per (row, head); scores over keys 0..pos in LDS.
 __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
                                                  float* __restrict__ o, int d, int H, int dh,
@@ -263,6 +428,27 @@ void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
                const int* nrows_dev, int nrows_cap, hipStream_t s) {
     if (f16) {
         if (nseg_cap <= 0) return;
+        // one wavefront per (segment, query block, head) once the launch has
+        // at least 2048 of them (8 per CU) and the page list fits a wavefront;
+        // below that, four wavefronts split each block's keys. The choice
+        // depends only on the launch's capacities, so Full and Compact rounds
+        // take the same kernel.
+        const int rows_blk = max_rows_per_seg <= 16 ? 16 : max_rows_per_seg <= 32 ? 32
+                           : max_rows_per_seg <= 48 ? 48 : 32;
+        const int qbl = (max_rows_per_seg + rows_blk - 1) / rows_blk;
+        if ((long)nseg_cap * qbl * heads >= 2048 && max_pages <= 64) {
+            const dim3 grid(nseg_cap * qbl, heads);
+            if (rows_blk == 16)
+                launch(k_attn_f16_seq<1>, grid, dim3(64), 0, s, (const uint16_t*)q, (uint16_t*)o, d,
+                       heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, qbl);
+            else if (rows_blk == 48)
+                launch(k_attn_f16_seq<3>, grid, dim3(64), 0, s, (const uint16_t*)q, (uint16_t*)o, d,
+                       heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, qbl);
+            else
+                launch(k_attn_f16_seq<2>, grid, dim3(64), 0, s, (const uint16_t*)q, (uint16_t*)o, d,
+                       heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, qbl);
+            return;
+        }
         if (max_rows_per_seg <= 16) {
             launch(k_attn_f16<1>, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
                    (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev, 1);
