@@ -15,6 +15,8 @@ Other modes:
   --peaks                 achievable copy and matmul rates (one JSON line)
   --copy-probe            one 1 GiB device-to-device copy, the calibration run
                           of the HBM byte counters
+  --mfma-probe            the library's MFMA calibration kernel: sustained
+                          rate, and the run the MFMA counters are read against
   --trace-summary DIR     per-class launch durations from the kernel trace CSV
                           that rocprofv3 --kernel-trace wrote under DIR
   --traffic-summary DIR   HBM bytes per launch and class from FETCH_SIZE and
@@ -448,6 +450,38 @@ def achievable_peaks() -> int:
     return 0
 
 
+def mfma_probe(launches: int = 10) -> int:
+    """The library's MFMA calibration kernel (one 256-thread workgroup per CU,
+    back-to-back independent 16x16x32 fp16 MFMAs, no memory traffic): its
+    sustained rate and the clock that rate implies at 4096 flops per CU per
+    cycle (the dense fp16 peak of 2.5 PFLOP/s at 256 CUs and 2.4 GHz)."""
+    import torch
+
+    import paper_2608_18183_amd as P
+    torch.cuda.set_device(0)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    iters = 32768
+    sink = torch.zeros(256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    flops = cus * 4 * iters * 8 * 16384.0
+    P.hbsjd_mfma_probe(cus, iters, sink, stream)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(launches):
+        P.hbsjd_mfma_probe(cus, iters, sink, stream)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    us = ev[0].elapsed_time(ev[1]) * 1e3 / launches
+    tf = flops / us / 1e6
+    print(json.dumps({"mfma_probe": {
+        "workgroups": cus, "wavefronts": 4 * cus, "iters": iters, "launches": launches,
+        "flops_per_launch": flops, "avg_launch_us": round(us, 2),
+        "tflops": round(tf, 1), "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4),
+        "implied_clock_ghz": round(tf * 1e12 / (cus * 4096.0) / 1e9, 3)}}), flush=True)
+    return 0
+
+
 def copy_probe() -> int:
     """One 1 GiB device-to-device copy after a fill: the run whose FETCH_SIZE
     and WRITE_SIZE readings give the counters' bytes per byte moved."""
@@ -764,6 +798,8 @@ def main() -> int:
                     help="measure achievable peaks instead (a 1 GiB device copy and "
                          "bf16 torch.matmul) and print them as one JSON line")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--mfma-probe", action="store_true",
+                    help="time the MFMA calibration kernel and print its rate as one JSON line")
     ap.add_argument("--trace-summary", metavar="DIR")
     ap.add_argument("--last", action="append", default=[], metavar="CLASS=N",
                     help="with --trace-summary: average CLASS over its last N launches")
@@ -783,6 +819,8 @@ def main() -> int:
         return achievable_peaks()
     if args.copy_probe:
         return copy_probe()
+    if args.mfma_probe:
+        return mfma_probe()
 
     import torch
 

@@ -334,6 +334,19 @@ hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t
                           void* stream);
 
 /*
+ * Measurement aid, not an operation of the method: a kernel that keeps the
+ * matrix cores busy for its whole run, for reading the MFMA counters against a
+ * known duty cycle and for the sustained MFMA rate. `workgroups` workgroups of
+ * four wavefronts each issue iters x 8 independent v_mfma_f32_16x16x32_f16
+ * (16384 flops each) back to back with no memory traffic, so one launch does
+ * workgroups x 4 x iters x 8 x 16384 flops. sink must point to 1 KB of
+ * writable device memory; the kernel writes it only if its sums take a value
+ * they cannot take. Asynchronous on `stream` (a hipStream_t, NULL = the null
+ * stream). Errors: EINVAL (workgroups < 1, iters < 1, sink NULL), EHIP.
+ */
+hbsjd_status hbsjd_mfma_probe(int32_t workgroups, int32_t iters, float* sink, void* stream);
+
+/*
  * Hardware calibration of the Full/Compact threshold (Sec. 4.3, Eq. 6): a
  * data-independent latency test. On synthetic state (`batch` images halfway
  * through an all-zero prefix of class 0, window `window`, no guidance) it

@@ -70,6 +70,7 @@ _SIGS = {
     "hbsjd_transform_rows_noalloc": (_I32, [_I32, _I32, _P, _I32, ctypes.c_float, _P, _I32,
                                             ctypes.c_uint64, _P, _P, _P, _P, _P]),
     "hbsjd_philox": (_I32, [ctypes.c_uint64, _I32, _P, _P, _P]),
+    "hbsjd_mfma_probe": (_I32, [_I32, _I32, _P, _P]),
     "hbsjd_calibrate_gamma": (_I32, [_P, _I32, _I32, _P]),
     "hbsjd_profile_start": (_I32, [_P, ctypes.c_uint32]),
     "hbsjd_profile_sample": (_I32, [_P, ctypes.c_int32]),
@@ -124,6 +125,8 @@ def _stream_handle(stream) -> Optional[int]:
         if not torch.cuda.is_available():
             return 0
         return torch.cuda.current_stream().cuda_stream
+    if hasattr(stream, "cuda_stream"):   # a torch.cuda.Stream
+        return stream.cuda_stream
     return int(stream)
 
 
@@ -359,6 +362,17 @@ def hbsjd_bikl_rows(logits_s, logits_t, stream=None):
     _check(L.hbsjd_bikl_rows(_P(_dev_ptr(logits_s)), _P(_dev_ptr(logits_t)), rows, V,
                              _P(_dev_ptr(out)), _P(_stream_handle(stream))), "hbsjd_bikl_rows")
     return out
+
+
+def hbsjd_mfma_probe(workgroups: int, iters: int, sink, stream=None):
+    """The MFMA calibration kernel (asynchronous on `stream`); sink: a device
+    tensor of at least 1 KB. One launch does workgroups x 4 x iters x 8 x 16384
+    flops."""
+    if sink.numel() * sink.element_size() < 1024:
+        raise ValueError("sink must hold at least 1 KB")
+    L = load_library()
+    _check(L.hbsjd_mfma_probe(int(workgroups), int(iters), _P(_dev_ptr(sink)),
+                              _P(_stream_handle(stream))), "hbsjd_mfma_probe")
 
 
 def hbsjd_philox(seed: int, bt, stream=None):

@@ -16,6 +16,11 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # packed fp32 instructions stay off: some of their forms have given
          # wrong results on this hardware without any error
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # MFMA accumulators in VGPRs: with the AGPR form the compiler moves
+         # loop-carried accumulators between AGPRs and VGPRs every K step
+         # (60-400 v_accvgpr moves per main-loop iteration of the smaller GEMM
+         # tiles and the attention kernels) and lowers their occupancy
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
 
 

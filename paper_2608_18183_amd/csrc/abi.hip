@@ -1446,6 +1446,19 @@ hbsjd_status hbsjd_philox(uint64_t seed, int32_t n, const uint32_t* bt, uint32_t
     }
 }
 
+hbsjd_status hbsjd_mfma_probe(int32_t workgroups, int32_t iters, float* sink, void* stream) {
+    try {
+        if (workgroups < 1 || iters < 1 || !sink) return fail(HBSJD_EINVAL, "bad mfma probe arguments");
+        hipStream_t s = (hipStream_t)stream;
+        mfma_probe(workgroups, iters, sink, s);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fail(HBSJD_EHIP, std::string("mfma probe: ") + hipGetErrorString(e));
+        return HBSJD_OK;
+    } catch (...) {
+        return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_mfma_probe");
+    }
+}
+
 hbsjd_status hbsjd_profile_start(hbsjd_ctx* c, uint32_t class_mask) {
     try {
         GUARD(c);

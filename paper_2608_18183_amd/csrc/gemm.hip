@@ -1239,4 +1239,34 @@ hipError_t gemm_setup() {
     return hipSuccess;
 }
 
+// ---------------------------------------------------------------- MFMA calibration
+// Every wavefront issues iters x 8 independent v_mfma_f32_16x16x32_f16 back to
+// back with no memory traffic: a kernel whose matrix cores are busy for its
+// whole run, against which the MFMA counters and the sustained rate are read.
+// The sums reach memory only if they equal a value they cannot take.
+__global__ __launch_bounds__(256) void k_mfma_probe(int iters, float* __restrict__ sink) {
+    const float x = (float)(threadIdx.x & 7) * 0.125f;
+    f16x8_t a, b;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        a[e] = (_Float16)(x + 0.25f * e);
+        b[e] = (_Float16)(0.5f - x);
+    }
+    f32x4_t acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[k], 0, 0, 0);
+    }
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += acc[k][0] + acc[k][1] + acc[k][2] + acc[k][3];
+    if (t == -1234567.f) sink[threadIdx.x] = t;
+}
+
+void mfma_probe(int workgroups, int iters, float* sink, hipStream_t s) {
+    launch(k_mfma_probe, dim3(workgroups), dim3(256), 0, s, iters, sink);
+}
+
 }  // namespace hbsjd
