@@ -889,6 +889,7 @@ hbsjd_status hbsjd_create(const hbsjd_model_desc* m, uint64_t max_kv_bytes, void
         c->max_kv_bytes = max_kv_bytes;
         hipError_t e = hipGetDevice(&c->device);
         if (e == hipSuccess) e = gemm_setup();
+        attention_setup();
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_user, hipEventDisableTiming);
         if (e != hipSuccess) {

@@ -15,6 +15,9 @@
 // fixed order. A row's result therefore depends only on its position and the
 // cache contents.
 // fp32 path: one wavefront per (row, head), two-pass softmax.
+#include <cstdlib>
+#include <cstring>
+
 #include "common.h"
 #include "launch.h"
 
@@ -422,6 +425,13 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
     }
 }
 
+static int g_force_attn = 0;   // HBSJD_ATTN_KERNEL: 1 "seq", -1 "split", 0 chosen per launch
+
+void attention_setup() {
+    const char* f = std::getenv("HBSJD_ATTN_KERNEL");
+    g_force_attn = !f ? 0 : std::strcmp(f, "seq") == 0 ? 1 : std::strcmp(f, "split") == 0 ? -1 : 0;
+}
+
 void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
                const void* kv_layer, const int32_t* ptab, int max_pages, const Segments& seg,
                const int* nseg_dev, int nseg_cap, int max_rows_per_seg, const RowMeta& rows,
@@ -436,7 +446,12 @@ void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
         const int rows_blk = max_rows_per_seg <= 16 ? 16 : max_rows_per_seg <= 32 ? 32
                            : max_rows_per_seg <= 48 ? 48 : 32;
         const int qbl = (max_rows_per_seg + rows_blk - 1) / rows_blk;
-        if ((long)nseg_cap * qbl * heads >= 2048 && max_pages <= 64) {
+        // (HBSJD_ATTN_KERNEL forces one kernel for every launch, for tests)
+        const bool seq_ok = max_pages <= 64;
+        const bool take_seq = g_force_attn > 0 ? seq_ok
+                            : g_force_attn < 0 ? false
+                            : (long)nseg_cap * qbl * heads >= 2048 && seq_ok;
+        if (take_seq) {
             const dim3 grid(nseg_cap * qbl, heads);
             if (rows_blk == 16)
                 launch(k_attn_f16_seq<1>, grid, dim3(64), 0, s, (const uint16_t*)q, (uint16_t*)o, d,

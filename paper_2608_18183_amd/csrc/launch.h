@@ -81,6 +81,8 @@ void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int
               const int* m_dev, int m_cap, const QkvArgs& e, hipStream_t s);
 // once per process before any launch (the wide GEMM's LDS allowance)
 hipError_t gemm_setup();
+// reads HBSJD_ATTN_KERNEL ("seq" / "split": one attention kernel for every launch)
+void attention_setup();
 // MFMA calibration kernel: workgroups x 4 wavefronts x iters x 8 MFMAs (16384 flops each)
 void mfma_probe(int workgroups, int iters, float* sink, hipStream_t s);
 // split-K partial sums part[split][m_cap][N] (tag 0: O projection, 1: W2);

@@ -290,6 +290,42 @@ def test_rollout_bf16_full_equals_compact_and_counts_are_bounded():
     assert (t0 >= 0).all() and (t0 < shape.vocab).all()
 
 
+@pytest.mark.parametrize("kernel", ["seq", "split"])
+def test_forward_bf16_each_attention_kernel_matches_oracle(kernel, monkeypatch):
+    """The two attention kernels (causal attention of each sequence's rows over
+    its own paged cache, Sec. 4.2): one wavefront walking a block's key tiles
+    in order, and four wavefronts splitting them and merging. A launch takes
+    one by its capacity; HBSJD_ATTN_KERNEL forces either on every launch. Both
+    meet the forward bar against the oracle on ragged prefill segments (1 to
+    256 rows: one to eight 32-row query blocks)."""
+    monkeypatch.setenv("HBSJD_ATTN_KERNEL", kernel)
+    _bf16_forward_case("llamagen_b", [40, 0, 90, 255, 17], 11)
+
+
+@pytest.mark.parametrize("W", [8, 16, 32])
+def test_rollout_bf16_full_equals_compact_sequential_attention(W, monkeypatch):
+    """Full and Compact rounds (Sec. 4.3) give identical tokens with the
+    sequential attention kernel on every launch, at windows of 9, 17 and 33
+    rows (one, two and three 16-row query groups per block)."""
+    monkeypatch.setenv("HBSJD_ATTN_KERNEL", "seq")
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 1, batch=8)
+    batch.prefix_len[3] = shape.T - 5
+    ctx = gu.make_ctx(shape, "bf16", blob)
+    outs = [ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                              batch.temperature, W, top_k=wl.top_k, seed=1000, exec_mode=mode,
+                              gamma=4)
+            for mode in [P().EXEC_FULL, P().EXEC_COMPACT]]
+    t0 = outs[0]["tokens"].cpu().numpy()
+    assert np.array_equal(outs[1]["tokens"].cpu().numpy(), t0)
+    assert np.array_equal(outs[1]["counts"].cpu().numpy(), outs[0]["counts"].cpu().numpy())
+    c = outs[0]["counts"].cpu().numpy()
+    for b in range(8):
+        assert c[:, b].sum() == shape.T - int(batch.prefix_len[b])
+
+
 # ------------------------------------------------------------------ cached-AR baseline
 
 
