@@ -350,9 +350,12 @@ hbsjd_status hbsjd_mfma_probe(int32_t workgroups, int32_t iters, float* sink, vo
  * Hardware calibration of the Full/Compact threshold (Sec. 4.3, Eq. 6): a
  * data-independent latency test. On synthetic state (`batch` images halfway
  * through an all-zero prefix of class 0, window `window`, no guidance) it
- * times the verifier forward in Full and in Compact mode with A = 1, 2, 4, ...,
- * batch images active, and returns the largest A at which Compact is no
- * slower. The context keeps it as the gamma of rollouts that pass gamma = -1.
+ * times the verifier forward in Full and in Compact mode with A = 1, 2, 4, ...
+ * (below batch) images active, and returns the largest A at which Compact is
+ * no slower (within 2% of Full, the timing noise); with every image active
+ * the two modes run the same rows, so gamma = batch when Compact was no
+ * slower at the largest A timed. The context keeps it as the gamma of
+ * rollouts that pass gamma = -1.
  * Rollout outputs never depend on gamma. Needs loaded weights; clears any
  * round-API state (a following hbsjd_round returns HBSJD_ESTATE). Errors:
  * EINVAL (batch < 1, window outside [1, 64], gamma NULL), ESTATE (no

@@ -217,10 +217,12 @@ __global__ __launch_bounds__(256) void k_attn_f16(const uint16_t* __restrict__ q
 
 // fp16, one wavefront per (segment, query block, head) when a launch has
 // enough of them to fill the chip: the wavefront walks its keys' 64-key tiles
-// in order with one online softmax, the K and V fragments of tile t + 1 in
-// flight while tile t is multiplied, and needs no LDS and no merge. The score
-// and probability layouts are those of k_attn_f16 (S^T = K Q^T, O^T = V^T P^T).
-// A row's result depends only on its position and the cache contents.
+// in order with one online softmax and needs no LDS and no merge. With 16- and
+// 32-query blocks the K and V fragments of tile t + 1 are in flight while tile
+// t is multiplied; a 48-query block holds one tile at a time, which keeps it at
+// two wavefronts per SIMD (XL rounds: 80 -> 63 us, the bits unchanged). The
+// score and probability layouts are those of k_attn_f16 (S^T = K Q^T,
+// O^T = V^T P^T). A row's result depends only on its position and the cache.
 template <int NMT>
 __global__ __launch_bounds__(64) void k_attn_f16_seq(const uint16_t* __restrict__ qb,
                                                      uint16_t* __restrict__ ob, int d, int H,
@@ -348,16 +350,25 @@ __global__ __launch_bounds__(64) void k_attn_f16_seq(const uint16_t* __restrict_
                                                                        0, 0, 0);
             }
     };
-    // two register buffers; every fetch is issued (the last tile re-fetched
-    // past the end), so the loads in flight are the same on every path
-    f16x8_t ka[4][2], va[4][2], kb[4][2], vb[4][2];
-    fetch(0, ka, va);
-    for (int tile = 0; tile < ntiles; tile += 2) {
-        fetch(min(tile + 1, ntiles - 1), kb, vb);
-        tile_step(tile, ka, va);
-        if (tile + 1 >= ntiles) break;
-        fetch(min(tile + 2, ntiles - 1), ka, va);
-        tile_step(tile + 1, kb, vb);
+    if constexpr (NMT >= 3) {
+        for (int tile = 0; tile < ntiles; ++tile) {
+            f16x8_t kc[4][2], vc[4][2];
+            fetch(tile, kc, vc);
+            tile_step(tile, kc, vc);
+        }
+    } else {
+        // two register buffers; every fetch is issued (the last tile
+        // re-fetched past the end), so the loads in flight are the same on
+        // every path
+        f16x8_t ka[4][2], va[4][2], kb[4][2], vb[4][2];
+        fetch(0, ka, va);
+        for (int tile = 0; tile < ntiles; tile += 2) {
+            fetch(min(tile + 1, ntiles - 1), kb, vb);
+            tile_step(tile, ka, va);
+            if (tile + 1 >= ntiles) break;
+            fetch(min(tile + 2, ntiles - 1), ka, va);
+            tile_step(tile + 1, kb, vb);
+        }
     }
 #pragma unroll
     for (int i = 0; i < NMT; ++i) {
