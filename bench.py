@@ -19,6 +19,9 @@ Other modes:
                           rate, and the run the MFMA counters are read against
   --trace-summary DIR     per-class launch durations from the kernel trace CSV
                           that rocprofv3 --kernel-trace wrote under DIR
+  --mfma-summary P T      MFMA counters per kernel class and tile (rocprofv3
+                          --pmc CSVs under P) against the durations traced
+                          under T by the same command
   --traffic-summary DIR   HBM bytes per launch and class from FETCH_SIZE and
                           WRITE_SIZE counter runs under DIR (copy_FETCH_SIZE,
                           copy_WRITE_SIZE, bench_FETCH_SIZE, bench_WRITE_SIZE),
@@ -346,6 +349,57 @@ def traffic_summary(dirpath, workload, out_path=TRAFFIC_JSON):
         json.dump(allrec, fh, indent=1)
         fh.write("\n")
     print(f"wrote {out_path} [{workload}]")
+    return 0
+
+
+def _variant(name: str) -> str:
+    if "k_gemm_wide" in name:
+        return "256x256"
+    m = re.search(r"k_gemm_f16<(\d+), (\d+)", name)
+    return f"{m.group(1)}x{m.group(2)}" if m else "-"
+
+
+def mfma_summary(pmc_dir, trace_dir, cus=256, xcds=8):
+    """MFMA counters per kernel class and tile, against traced durations of
+    the same command. Executed MFMA flops = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512;
+    MfmaUtil = sum of SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / xcds x
+    4 x cus SIMDs), since GRBM_GUI_ACTIVE reads the cycles of all XCDs summed
+    (what the calibration kernel, busy on every SIMD for its whole run, shows)."""
+    vals, names = {}, {}
+    for r in csv.DictReader(open(_find(pmc_dir, "counter_collection.csv"))):
+        i = int(r["Dispatch_Id"])
+        vals.setdefault(i, {}).setdefault(r["Counter_Name"], 0.0)
+        vals[i][r["Counter_Name"]] += float(r["Counter_Value"])
+        names[i] = r["Kernel_Name"]
+    dur = {}
+    for r in csv.DictReader(open(_find(trace_dir, "kernel_trace.csv"))):
+        key = (r["Kernel_Name"], )
+        dur.setdefault(key, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    rows = {}
+    for i, v in vals.items():
+        cls, _ = kernel_class(names[i])
+        if cls is None:
+            cls = "mfma_probe" if "k_mfma_probe" in names[i] else "other"
+        key = (cls, _variant(names[i]), names[i])
+        agg = rows.setdefault(key, {"n": 0})
+        agg["n"] += 1
+        for c, x in v.items():
+            agg[c] = agg.get(c, 0.0) + x
+    print(f"MFMA counters ({pmc_dir}) against traced durations ({trace_dir}); "
+          f"MfmaUtil = busy / (GRBM_GUI_ACTIVE / {xcds} x {4 * cus} SIMDs)")
+    print(f"{'class':11s} {'tile':8s} {'dispatches':>10s} {'avg us':>9s} {'GFLOP/disp':>11s} "
+          f"{'TFLOP/s':>8s} {'of peak':>8s} {'MfmaUtil':>9s}")
+    for (cls, var, name), a in sorted(rows.items()):
+        ds = dur.get((name, ), [])
+        if not ds or "SQ_INSTS_VALU_MFMA_MOPS_F16" not in a:
+            continue
+        n = a["n"]
+        fl = a["SQ_INSTS_VALU_MFMA_MOPS_F16"] * 512.0 / n
+        us = sum(ds) / len(ds) / 1e3
+        util = a["SQ_VALU_MFMA_BUSY_CYCLES"] / (a["GRBM_GUI_ACTIVE"] / xcds * 4 * cus)
+        tf = fl / us / 1e6
+        print(f"{cls:11s} {var:8s} {n:10d} {us:9.2f} {fl / 1e9:11.3f} {tf:8.1f} "
+              f"{tf / MFMA_PEAK_TFLOPS:8.4f} {util:9.4f}")
     return 0
 
 
@@ -805,12 +859,17 @@ def main() -> int:
     ap.add_argument("--last", action="append", default=[], metavar="CLASS=N",
                     help="with --trace-summary: average CLASS over its last N launches")
     ap.add_argument("--traffic-summary", metavar="DIR")
+    ap.add_argument("--mfma-summary", nargs=2, metavar=("PMC_DIR", "TRACE_DIR"),
+                    help="MFMA counters (SQ_INSTS_VALU_MFMA_MOPS_F16, SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "GRBM_GUI_ACTIVE) per class and tile against traced durations")
     args = ap.parse_args()
     if args.trace_summary:
         return trace_summary(args.trace_summary,
                              {c: int(n) for c, n in (x.split("=") for x in args.last)})
     if args.traffic_summary:
         return traffic_summary(args.traffic_summary, args.workload)
+    if args.mfma_summary:
+        return mfma_summary(*args.mfma_summary)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the rollout "
               f"shards by image with no cross-GPU exchange, so each GPU would run its own "

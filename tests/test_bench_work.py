@@ -155,3 +155,34 @@ def test_traffic_summary_scales_by_the_copy_and_sums_paired_dispatches(tmp_path)
     assert w13["fetch_kib_per_launch"] == 100.0 and w13["write_kib_per_launch"] == 32.0
     assert w13["hbm_bytes_per_launch"] == int(100 * 1024 / 0.5 + 32 * 1024)
     assert rec["wl"]["attn"]["hbm_bytes_per_launch"] == int(10 * 1024 / 0.5 + 5 * 1024)
+
+
+def test_mfma_summary_normalises_grbm_by_the_xcds(tmp_path, capsys):
+    """MfmaUtil divides the summed busy cycles by GRBM_GUI_ACTIVE / 8 (the
+    cycles of the 8 XCDs summed) times the SIMDs: a kernel whose MFMA
+    instructions kept every SIMD busy for a third of its cycles reads 1/3,
+    the same as its flop rate against the peak at 2.4 GHz."""
+    import csv
+    cus, clk = 256, 2.4e9
+    secs = 1e-3
+    grbm = 8 * secs * clk                      # all XCDs' cycles
+    busy = secs * clk * 4 * cus / 3            # a third of every SIMD's cycles
+    mops = busy * 2                            # 16 busy cycles per 8192-MOP MFMA
+    (tmp_path / "p").mkdir()
+    (tmp_path / "t").mkdir()
+    name = "hbsjd::k_mfma_probe(int, float*)"
+    with open(tmp_path / "p" / "run_counter_collection.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for c, v in [("SQ_INSTS_VALU_MFMA_MOPS_F16", mops), ("SQ_VALU_MFMA_BUSY_CYCLES", busy),
+                     ("GRBM_GUI_ACTIVE", grbm)]:
+            w.writerow([1, name, c, v])
+    with open(tmp_path / "t" / "run_kernel_trace.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writerow([name, 0, int(secs * 1e9)])
+    assert bench.mfma_summary(str(tmp_path / "p"), str(tmp_path / "t"), cus=cus) == 0
+    row = [ln for ln in capsys.readouterr().out.splitlines() if ln.startswith("mfma_probe")][0]
+    frac, util = float(row.split()[-2]), float(row.split()[-1])
+    assert abs(util - 1 / 3) < 1e-4
+    assert abs(frac - (mops * 512 / secs) / 2.5e15) < 1e-4
