@@ -170,7 +170,9 @@ struct EpiQkv {
     // written by NT threads. q and K: each thread takes 8 consecutive columns
     // (four pairs of one head) of a row, fetches their four cos and four sin
     // values as two 16-byte loads, turns the pairs and stores 16 bytes. V^T:
-    // each thread a row (= cache slot) and a strided set of dimensions.
+    // each thread a row (= cache slot) and a strided set of dimensions, in
+    // groups of RH threads, as many groups as a power of two that fits in NT
+    // (4 groups for RH = 128 or 96, 8 for 64).
     template <int BT, int RH, int NT>
     __device__ void store_rows_f32(const float* tile, int ld, int n0, int m0, int rb, int M) const {
         const int t = threadIdx.x;
@@ -178,6 +180,7 @@ struct EpiQkv {
         const int head = c0 >> 6;
         if (part < 2) {
             constexpr int kChunks = BT / 8;
+            static_assert(RH * kChunks % NT == 0, "q and K chunks per thread");
 #pragma unroll
             for (int h = 0; h < RH * kChunks / NT; ++h) {
                 const int qd = t + NT * h, r = qd / kChunks, col = (qd % kChunks) * 8;
@@ -203,9 +206,10 @@ struct EpiQkv {
                 *reinterpret_cast<u32x4_t*>(dst) = out;
             }
         } else {
-            constexpr int kGroups = NT / RH;
+            constexpr int kGroups = NT / RH >= 8 ? 8 : NT / RH >= 4 ? 4 : NT / RH >= 2 ? 2 : 1;
+            static_assert(BT % kGroups == 0, "V^T columns per thread");
             const int r = t % RH, m = m0 + rb + r;
-            if (m < M) {
+            if (t < kGroups * RH && m < M) {
                 const Row ri = row_info(m);
                 T* dst = kv + ri.off + head * 64 * 64;
 #pragma unroll 8
@@ -305,6 +309,7 @@ struct EpiSwiGLU {
     template <int BT, int TR = BT, int NT = 256>
     __device__ void store_tile(const uint16_t* tile, int n0, int m0, int M) const {
         constexpr int kChunks = BT / 16;   // 16-byte chunks per row of BT / 2 outputs
+        static_assert(TR * kChunks % NT == 0, "chunks per thread");
         const int t = threadIdx.x, ldt = tile_ld<BT>();
 #pragma unroll
         for (int h = 0; h < TR * kChunks / NT; ++h) {
@@ -417,18 +422,38 @@ __device__ __forceinline__ void wait_loads() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
-// Which of a wide-tile launch and the 128 x 128 launch beside it does the
-// work, from the rows present (read on the device): rounds of tiles per CU
-// times a per-tile time fitted to measured launches (hundredths of a
-// microsecond per 64-deep step, plus a fixed part): 256 x 256 tiles one per
-// CU at 9 + 1.35 s us, 128 x 128 tiles two per CU at 17.4 + 0.6 s us. Both
-// kernels evaluate it in the same integer arithmetic, so exactly one works.
-__host__ __device__ inline bool wide_works(int M, int N, int K, int splits, int cus) {
+// The wide kernel's tile height (32 TM rows by 256 columns, TM = 8, 6 or 4)
+// and which of it and the 128 x 128 launch beside it does the work, from the
+// rows present (read on the device). Each candidate costs its rounds of
+// tiles times a per-round time, fitted (within 7% on average) to launches of
+// the five XL products at 132-8448 rows, in hundredths of a microsecond with
+// s 64-deep steps per tile: wide tiles one per CU, dealt per XCD, at
+// 19.1 + 1.26 s (TM 8), 11.7 + 1.08 s (TM 6) and 7.9 + 0.84 s (TM 4);
+// 128 x 128 tiles one per CU at 6.6 + 0.46 s, plus 4.4 per launch. Both
+// kernels evaluate it in the same integer arithmetic, so exactly one works;
+// ties go to the wide kernel and the taller tile. Returns TM, or 0 when the
+// 128 x 128 kernel works (never with small = false).
+__host__ __device__ inline long wide_cost(int tm, int M, int N, int s, int splits, int cus) {
+    const int rows = 32 * tm;
+    const long tiles = (long)((M + rows - 1) / rows) * (N / 256) * splits;
+    const long slots = cus / 8, rounds = ((tiles + 7) / 8 + slots - 1) / slots;
+    const long fixed = tm == 8 ? 1910 : tm == 6 ? 1170 : 790;
+    const long step = tm == 8 ? 126 : tm == 6 ? 108 : 84;
+    return rounds * (fixed + step * s);
+}
+__host__ __device__ inline int wide_pick(int M, int N, int K, int splits, int cus, bool small) {
     const int s = K / splits / 64;
-    const long t256 = (long)((M + 255) / 256) * (N / 256) * splits;
     const long t128 = (long)((M + 127) / 128) * (N / 128) * splits;
-    const long rw = (t256 + cus - 1) / cus, rf = (t128 + 2 * cus - 1) / (2 * cus);
-    return rw * (900 + 135 * s) <= rf * (1740 + 60 * s);
+    long best = small ? 440 + (t128 + cus - 1) / cus * (660 + 46 * s) : -1;
+    int pick = 0;
+    for (int tm = 8; tm >= 4; tm -= 2) {
+        const long c = wide_cost(tm, M, N, s, splits, cus);
+        if (best < 0 || (pick == 0 ? c <= best : c < best)) {
+            best = c;
+            pick = tm;
+        }
+    }
+    return pick;
 }
 
 template <int BM, int BN, int WGM, int WGN, int NS, bool kDirect, typename Epi>
@@ -447,8 +472,8 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
 
     const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
     // launched beside the wide kernel (pair_cus = the CU count): the one of
-    // the two that wide_works picks does the work
-    if (pair_cus > 0 && wide_works(M, N, K, splits, pair_cus)) return;
+    // the two that wide_pick picks does the work
+    if (pair_cus > 0 && wide_pick(M, N, K, splits, pair_cus, true) != 0) return;
     if (M <= 0) return;
     // Persistent: the grid holds about as many workgroups as the CUs keep
     // resident, and each loops over tiles. The tiles of the rows present are
@@ -734,7 +759,10 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
 }
 
 static int g_cus = 256;   // compute units of the device (gemm_setup)
-static int g_force_tile = 0;   // HBSJD_GEMM_TILE: 1 "wide", -1 "small", 0 chosen per launch
+// HBSJD_GEMM_TILE: "wide" (1), "wide256" / "wide192" / "wide128" (1, with the
+// wide kernel's tile height fixed), "small" (-1); unset: chosen per launch (0)
+static int g_force_tile = 0;
+static int g_force_tm = 0;   // the forced height as TM (32 TM rows), 0 chosen per launch
 
 // workgroups of a 256-thread kernel one CU holds at once (looked up once per
 // kernel; at least 1)
@@ -751,34 +779,42 @@ static int resident(const void* kern) {
 }
 
 // ---------------------------------------------------------------- wide tile
-// Launches with at least one 256 x 256 tile per CU take this kernel: 512
-// threads as 2 x 4 wavefronts, each a 128 x 64 block of 8 x 4
-// v_mfma_f32_16x16x32_f16 tiles whose 32 accumulators live in VGPRs (two
-// wavefronts per SIMD share the register file; a 128 x 128 block per
-// wavefront would fill all 256 AGPRs and the compiler then shuffles
+// Launches with enough rows take this kernel: 512 threads as 2 x 4
+// wavefronts over a tile of 32 TM rows by 256 columns, TM = 8, 6 or 4 (256,
+// 192 or 128 rows) chosen per launch by wide_pick. Each wavefront holds a
+// 16 TM x 64 block of TM x 4 v_mfma_f32_16x16x32_f16 tiles whose accumulators
+// live in VGPRs (two wavefronts per SIMD share the register file; a 128 x 128
+// block per wavefront would fill all 256 AGPRs and the compiler then shuffles
 // accumulators through VGPRs every step, measured at 0.31 of the MFMA rate
 // against 0.47 for two 128 x 64 blocks). K advances 64 deep per step through
-// two 64 KB LDS stages filled straight from global memory (rows of eight
-// 16-byte chunks, chunk c of row r at c ^ (r & 7)): the loads of step k+1 are
-// issued when step k starts. Tiles are dealt so that each XCD's concurrent
-// workgroups cover about 4 row tiles x 8 column tiles, which its L2 serves
-// from one read of each operand slice. Split-K, wscale and the epilogues are those
-// of k_gemm_f16; staged epilogues stage the whole 256 x 256 tile in LDS.
-constexpr int kWideM = 256, kWideN = 256, kWideK = 64;
-constexpr int kWideStage = (kWideM + kWideN) * kWideK * 2;    // 64 KB
-constexpr int kWideLds = kWideM * (kWideN + 8) * 2;           // the staged tile (> 2 stages)
-static_assert(kWideLds >= 2 * kWideStage && kWideLds >= kWideM / 2 * (kWideN + 4) * 4,
+// two LDS stages (64 KB each at TM = 8) filled straight from global memory
+// (rows of eight 16-byte chunks, chunk c of row r at c ^ (r & 7)): the loads
+// of step k+1 are issued when step k starts. Tiles are dealt so that each
+// XCD's concurrent workgroups cover about 4 row tiles x 8 column tiles, which
+// its L2 serves from one read of each operand slice. Shorter tiles fill more
+// CUs when a launch has few of them: 1280 output columns at 8448 rows make
+// 165 tiles of 256 rows for 256 CUs but 220 of 192 rows. Every output element
+// sums its K products in the same order at every height, so rows are
+// bit-identical across heights and with k_gemm_f16. Split-K, wscale and the
+// epilogues are those of k_gemm_f16; staged epilogues stage the whole tile in
+// LDS.
+constexpr int kWideN = 256, kWideK = 64;
+constexpr int wide_rows(int tm) { return 32 * tm; }
+constexpr int wide_stage(int tm) { return (wide_rows(tm) + kWideN) * kWideK * 2; }   // bytes
+constexpr int kWideLds = wide_rows(8) * (kWideN + 8) * 2;   // the staged TM = 8 tile (> 2 stages)
+static_assert(kWideLds >= 2 * wide_stage(8) && kWideLds >= wide_rows(8) / 2 * (kWideN + 4) * 4,
               "LDS of the wide kernel");
 
-template <typename Epi>
-__global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict__ A, int lda,
-                                                      const uint16_t* __restrict__ W, float wscale,
-                                                      int N, int K, const int* __restrict__ m_dev,
-                                                      int m_cap, int splits, int pair_cus,
-                                                      float* __restrict__ part, Epi epi) {
-    constexpr int TM = 8, TN = 4, WM = TM * 16, WN = TN * 16;
-    constexpr int LPW = (kWideM + kWideN) / 8 / 8;   // 16-byte loads per wavefront per stage
-    extern __shared__ __attribute__((aligned(1024))) uint16_t smem[];
+// the persistent tile loop of k_gemm_wide at tile height 32 TM
+template <int TM, typename Epi>
+__device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __restrict__ A, int lda,
+                                           const uint16_t* __restrict__ W, float wscale, int M,
+                                           int N, int K, int m_cap, int splits,
+                                           float* __restrict__ part, const Epi& epi) {
+    constexpr int TN = 4, WM = TM * 16, WN = TN * 16;
+    constexpr int kRows = wide_rows(TM), kStage = wide_stage(TM) / 2;   // stage in elements
+    constexpr int LPW = (kRows + kWideN) / 8 / 8;   // 16-byte loads per wavefront per stage
+    static_assert(TM % 2 == 0 && TM >= 4 && TM <= 8, "tile heights of 128, 192 and 256 rows");
 
     // Persistent: the grid has at most one workgroup per CU (G of them, a
     // multiple of 8, dealt to the XCDs round-robin) and each loops over
@@ -787,12 +823,8 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
     // x takes the x-th contiguous eighth of that order and its G / 8
     // workgroups stride through it, so the concurrent tiles of an XCD share
     // operand slices in its L2 and every XCD gets an equal share however few
-    // rows are present. Launched beside k_gemm_f16 (pair_cus = the CU count),
-    // it works only when wide_works picks it.
-    const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
-    if (M <= 0) return;
-    const int tiles_m = (M + kWideM - 1) / kWideM, tiles_n = N / kWideN;
-    if (pair_cus > 0 && !wide_works(M, N, K, splits, pair_cus)) return;
+    // rows are present.
+    const int tiles_m = (M + kRows - 1) / kRows, tiles_n = N / kWideN;
     const int total = tiles_m * tiles_n * splits;
     const int per_xcd = (total + 7) >> 3;
     const int xcd = (int)(blockIdx.x & 7), slot = (int)(blockIdx.x >> 3);
@@ -818,7 +850,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const int r = wn * WN + j * 16 + fr;
-            boff[h][j] = kWideM * kWideK + r * kWideK + (((4 * h + fc) ^ (r & 7)) << 3);
+            boff[h][j] = kRows * kWideK + r * kWideK + (((4 * h + fc) ^ (r & 7)) << 3);
         }
     }
 
@@ -828,7 +860,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
         const int gsz = min(tiles_m - first, kGroup);
         const int in = tl - grp * kGroup * tiles_n;
         const int tm = first + in % gsz, tn = in / gsz;
-        const int m0 = tm * kWideM, n0 = tn * kWideN;
+        const int m0 = tm * kRows, n0 = tn * kWideN;
         const int kbase = z * Ks;
 
         // wavefront wv loads 8-row blocks wv, wv + 8, ... of A then of W
@@ -836,14 +868,14 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
 #pragma unroll
         for (int i = 0; i < LPW; ++i) {
             const int f = wv + 8 * i;
-            const int r = 8 * (f < kWideM / 8 ? f : f - kWideM / 8) + lr;
+            const int r = 8 * (f < kRows / 8 ? f : f - kRows / 8) + lr;
             const int c = (lp ^ (r & 7)) * 8;
-            src[i] = f < kWideM / 8 ? A + (size_t)min(m0 + r, M - 1) * lda + kbase + c
+            src[i] = f < kRows / 8 ? A + (size_t)min(m0 + r, M - 1) * lda + kbase + c
                                     : W + (size_t)(n0 + r) * K + kbase + c;
         }
         auto issue = [&](int kt, int st) {
             kt = kt < nk ? kt : nk - 1;
-            uint16_t* sb = smem + st * (kWideStage / 2);
+            uint16_t* sb = smem + st * kStage;
 #pragma unroll
             for (int i = 0; i < LPW; ++i) load_to_lds16(src[i] + kt * kWideK, sb + (wv + 8 * i) * 512);
         };
@@ -860,7 +892,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
             wait_loads<0>();
             lds_barrier();
             issue(kt + 1, (kt + 1) & 1);   // the last step re-reads its own tile into the idle stage
-            const uint16_t* sb = smem + (kt & 1) * (kWideStage / 2);
+            const uint16_t* sb = smem + (kt & 1) * kStage;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 f16x8_t a[TM], b[TN];
@@ -912,7 +944,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
         Epi e = epi;
         e.begin_tile(n0);
         if constexpr (epi_stages_f32<Epi>(0)) {
-            // two passes of 128 rows (the wavefronts of one wm each) in fp32
+            // two passes of 16 TM rows (the wavefronts of one wm each) in fp32
             constexpr int kLd = kWideN + 4;
             float* ft = reinterpret_cast<float*>(smem);
 #pragma unroll
@@ -929,7 +961,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
                                     acc[i][j][v];
                 }
                 __syncthreads();
-                e.template store_rows_f32<kWideN, kWideM / 2, 512>(ft, kLd, n0, m0, half * (kWideM / 2), M);
+                e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M);
             }
             continue;
         } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
@@ -960,7 +992,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
                 }
             }
             __syncthreads();
-            e.template store_tile<kWideN, kWideM, 512>(smem, n0, m0, M);
+            e.template store_tile<kWideN, kRows, 512>(smem, n0, m0, M);
             continue;
         }
 #pragma unroll
@@ -981,6 +1013,30 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
     }
 }
 
+template <typename Epi>
+__global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict__ A, int lda,
+                                                      const uint16_t* __restrict__ W, float wscale,
+                                                      int N, int K, const int* __restrict__ m_dev,
+                                                      int m_cap, int splits, int pair_cus,
+                                                      int force_tm, float* __restrict__ part,
+                                                      Epi epi) {
+    extern __shared__ __attribute__((aligned(1024))) uint16_t smem[];
+    const int M = m_dev ? min(*m_dev, m_cap) : m_cap;
+    if (M <= 0) return;
+    // Launched beside k_gemm_f16 (pair_cus = the CU count) it works only when
+    // wide_pick picks it; alone it picks the height among its own. A nonzero
+    // force_tm fixes the height (the results are the same).
+    const int pick = wide_pick(M, N, K, splits, pair_cus > 0 ? pair_cus : (int)gridDim.x, pair_cus > 0);
+    if (pick == 0) return;
+    const int tm = force_tm ? force_tm : pick;
+    if (tm == 4)
+        wide_tiles<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+    else if (tm == 6)
+        wide_tiles<6>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+    else
+        wide_tiles<8>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+}
+
 // the wide kernel needs more than 64 KB of dynamic LDS: allowed once per
 // epilogue type (at library set-up, before any graph capture)
 template <typename Epi>
@@ -993,11 +1049,13 @@ template <typename Epi>
 static void launch_wide(const void* A, int lda, const void* W, float wscale, int N, int K,
                         const int* m_dev, int m_cap, int splits, int pair_cus, float* part,
                         const Epi& epi, hipStream_t s) {
-    const int tiles = ((m_cap + kWideM - 1) / kWideM) * (N / kWideN) * splits;
+    // sized for the capacity's tiles at the smallest height
+    const int tiles = ((m_cap + wide_rows(4) - 1) / wide_rows(4)) * (N / kWideN) * splits;
     const int cap = (g_cus / 8) * 8;
     const int grid = std::max(8, std::min(cap, ((tiles + 7) / 8) * 8));
     launch(k_gemm_wide<Epi>, dim3(grid), dim3(512), (uint32_t)kWideLds, s, (const uint16_t*)A, lda,
-           (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits, pair_cus, part, epi);
+           (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits, pair_cus, g_force_tm, part,
+           epi);
 }
 
 template <int BM, int BN, int WGM, int WGN, typename Epi>
@@ -1037,7 +1095,7 @@ static void launch_f16(const void* A, int lda, const void* W, float wscale, int 
 // large tiles once there are enough of them to fill the 256 CUs twice over
 // Launches whose rows are only known on the device (m_dev) and that could
 // fill the wide kernel take both it and the smaller-tile kernel; each reads
-// the row count and wide_works tells which one works. (A persistent launch
+// the row count and wide_pick tells which one works. (A persistent launch
 // that finds no work costs a few microseconds; a wide-tile launch sized for
 // the capacity would cost its idle workgroups' dispatch, about as much as
 // the work of a full launch.)
@@ -1062,7 +1120,7 @@ static void dispatch_f16(const void* A, int lda, const void* W, float wscale, in
     }
     const bool wide = fit && t256 >= kWideMin;
     if (wide && !m_dev) {   // the rows are known here: the same choice on the host
-        if (wide_works(m_cap, N, K, splits, g_cus)) {
+        if (wide_pick(m_cap, N, K, splits, g_cus, true) != 0) {
             launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
             return;
         }
@@ -1238,7 +1296,17 @@ static_assert(epi_stages_f32<EpiQkv<uint16_t>>(0) && !epi_stages_f32<EpiSwiGLU<u
 
 hipError_t gemm_setup() {
     const char* f = std::getenv("HBSJD_GEMM_TILE");
-    g_force_tile = !f ? 0 : std::strcmp(f, "wide") == 0 ? 1 : std::strcmp(f, "small") == 0 ? -1 : 0;
+    g_force_tile = 0;
+    g_force_tm = 0;
+    if (f) {
+        const struct { const char* name; int tile, tm; } opts[] = {
+            {"wide", 1, 0}, {"wide256", 1, 8}, {"wide192", 1, 6}, {"wide128", 1, 4}, {"small", -1, 0}};
+        for (const auto& o : opts)
+            if (std::strcmp(f, o.name) == 0) {
+                g_force_tile = o.tile;
+                g_force_tm = o.tm;
+            }
+    }
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&

@@ -681,12 +681,15 @@ def test_profile_sampling_brackets_one_launch_in_every(tiny):
 
 @pytest.mark.parametrize("name", ["stress_b", "llamagen_xl_cfg"])
 def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
-    """Every projection may run on the wide 256 x 256 kernel or on the 128 x 128
-    / 64 x 64 one, chosen per launch from the rows present; Full and Compact
+    """Every projection may run on the wide kernel (tiles of 256, 192 or 128 rows
+    by 256 columns) or on the 128 x 128 / 64 x 64 one, chosen per launch from
+    the rows present; Full and Compact
     rounds (Sec. 4.3) process the same row in launches of different sizes, so
     the kernels must agree bit for bit. Forward logits of the same sequences
-    with every launch forced onto one kernel (HBSJD_GEMM_TILE) and chosen per
-    launch must be identical, at a row count where the choice varies."""
+    with every launch forced onto one kernel (HBSJD_GEMM_TILE: the wide kernel
+    at its chosen tile height or at 256, 192 or 128 rows, or the small-tile
+    kernel) and chosen per launch must be identical, at a row count where the
+    choice varies."""
     wl = synth.WORKLOADS[name]
     shape = wl.model
     blob = synth.make_weights(shape, 0, std=wl.weight_std, bias_std=wl.bias_std)
@@ -697,7 +700,7 @@ def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
     toks = rng.integers(0, shape.vocab, size=(n, shape.T)).astype(np.int32)
     labels = rng.integers(0, shape.n_classes + 1, size=n).astype(np.int32)
     outs = {}
-    for force in ["wide", "small", ""]:
+    for force in ["wide", "wide256", "wide192", "wide128", "small", ""]:
         if force:
             monkeypatch.setenv("HBSJD_GEMM_TILE", force)
         else:
@@ -707,5 +710,5 @@ def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
                                         labels).cpu().numpy()
         del ctx
     monkeypatch.delenv("HBSJD_GEMM_TILE", raising=False)
-    assert np.array_equal(outs["wide"].view(np.uint32), outs["small"].view(np.uint32))
-    assert np.array_equal(outs[""].view(np.uint32), outs["small"].view(np.uint32))
+    for force, out in outs.items():
+        assert np.array_equal(out.view(np.uint32), outs["small"].view(np.uint32)), force
