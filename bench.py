@@ -354,7 +354,7 @@ def traffic_summary(dirpath, workload, out_path=TRAFFIC_JSON):
 
 def _variant(name: str) -> str:
     if "k_gemm_wide" in name:
-        return "256x256"
+        return "wide"   # 256, 192 or 128 rows by 256 columns, chosen per launch
     m = re.search(r"k_gemm_f16<(\d+), (\d+)", name)
     return f"{m.group(1)}x{m.group(2)}" if m else "-"
 
