@@ -188,4 +188,20 @@ __device__ inline float block_reduce(float v, float* red, F op) {
     return r;
 }
 
+// one 16-byte chunk per lane from global memory to LDS: lane l's chunk lands
+// at lds + 16 l (lds is the same for the whole wavefront)
+__device__ __forceinline__ void load_to_lds16(const void* g, void* lds) {
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+// workgroup barrier alone; the memory clobber keeps the compiler from moving
+// LDS accesses across it
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// wait until at most N vector memory loads of this wavefront are outstanding
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    // s_waitcnt fields: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at [15:14]
+    __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
 }  // namespace hbsjd

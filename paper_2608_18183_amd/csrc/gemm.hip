@@ -406,21 +406,6 @@ constexpr auto epi_stages_f32(int) -> decltype(&E::template store_rows_f32<256, 
 template <typename E>
 constexpr bool epi_stages_f32(long) { return false; }
 
-// one 16-byte chunk per lane from global memory to LDS: lane l's chunk lands
-// at lds + 16 l (lds is the same for the whole wavefront)
-__device__ __forceinline__ void load_to_lds16(const void* g, void* lds) {
-    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-// workgroup barrier alone; the memory clobber keeps the compiler from moving
-// LDS accesses across it
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
-// wait until at most N vector memory loads of this wavefront are outstanding
-template <int N>
-__device__ __forceinline__ void wait_loads() {
-    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
-    // s_waitcnt fields: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at [15:14]
-    __builtin_amdgcn_s_waitcnt((N & 15) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
-}
 
 // The wide kernel's tile height (32 TM rows by 256 columns, TM = 8, 6 or 4)
 // and which of it and the 128 x 128 launch beside it does the work, from the
@@ -429,28 +414,38 @@ __device__ __forceinline__ void wait_loads() {
 // the five XL products at 132-8448 rows, in hundredths of a microsecond with
 // s 64-deep steps per tile: wide tiles one per CU, dealt per XCD, at
 // 19.1 + 1.26 s (TM 8), 11.7 + 1.08 s (TM 6) and 7.9 + 0.84 s (TM 4);
-// 128 x 128 tiles one per CU at 6.6 + 0.46 s, plus 4.4 per launch. Both
-// kernels evaluate it in the same integer arithmetic, so exactly one works;
-// ties go to the wide kernel and the taller tile. Returns TM, or 0 when the
-// 128 x 128 kernel works (never with small = false).
+// 128 x 128 tiles one per CU at 6.6 + 0.46 s, plus 4.4 per launch. One more
+// candidate, kWideHalfTail: 256-row tiles whose last round, when at most half
+// full, runs as 128-row halves (full rounds at the 256-row time, that round
+// at the 128-row time). Both kernels evaluate it in the same integer
+// arithmetic, so exactly one works; ties go to the wide kernel and to the
+// earlier candidate in the order 256 rows, half tail, 192, 128. Returns TM
+// (or kWideHalfTail), or 0 when the 128 x 128 kernel works (never with
+// small = false).
+constexpr int kWideHalfTail = 9;
 __host__ __device__ inline long wide_cost(int tm, int M, int N, int s, int splits, int cus) {
-    const int rows = 32 * tm;
+    const int rows = 32 * (tm == kWideHalfTail ? 8 : tm);
     const long tiles = (long)((M + rows - 1) / rows) * (N / 256) * splits;
-    const long slots = cus / 8, rounds = ((tiles + 7) / 8 + slots - 1) / slots;
-    const long fixed = tm == 8 ? 1910 : tm == 6 ? 1170 : 790;
-    const long step = tm == 8 ? 126 : tm == 6 ? 108 : 84;
-    return rounds * (fixed + step * s);
+    const long slots = cus / 8, per_xcd = (tiles + 7) / 8;
+    const long t8 = 1910 + 126 * s, t6 = 1170 + 108 * s, t4 = 790 + 84 * s;
+    if (tm == kWideHalfTail) {
+        const long full = per_xcd / slots, rest = per_xcd - full * slots;
+        return rest > 0 && 2 * rest <= slots ? full * t8 + t4 : -1;   // -1: not a candidate
+    }
+    return (per_xcd + slots - 1) / slots * (tm == 8 ? t8 : tm == 6 ? t6 : t4);
 }
 __host__ __device__ inline int wide_pick(int M, int N, int K, int splits, int cus, bool small) {
     const int s = K / splits / 64;
     const long t128 = (long)((M + 127) / 128) * (N / 128) * splits;
     long best = small ? 440 + (t128 + cus - 1) / cus * (660 + 46 * s) : -1;
     int pick = 0;
-    for (int tm = 8; tm >= 4; tm -= 2) {
-        const long c = wide_cost(tm, M, N, s, splits, cus);
+    const int order[4] = {8, kWideHalfTail, 6, 4};
+    for (int k = 0; k < 4; ++k) {
+        const long c = wide_cost(order[k], M, N, s, splits, cus);
+        if (c < 0) continue;
         if (best < 0 || (pick == 0 ? c <= best : c < best)) {
             best = c;
-            pick = tm;
+            pick = order[k];
         }
     }
     return pick;
@@ -760,9 +755,11 @@ __global__ __launch_bounds__(256) void k_gemm_f16(const uint16_t* __restrict__ A
 
 static int g_cus = 256;   // compute units of the device (gemm_setup)
 // HBSJD_GEMM_TILE: "wide" (1), "wide256" / "wide192" / "wide128" (1, with the
-// wide kernel's tile height fixed), "small" (-1); unset: chosen per launch (0)
+// wide kernel's tile height fixed), "wide256h" (1, 256-row tiles with the
+// half-height last round whenever it applies), "small" (-1); unset: chosen
+// per launch (0)
 static int g_force_tile = 0;
-static int g_force_tm = 0;   // the forced height as TM (32 TM rows), 0 chosen per launch
+static int g_force_tm = 0;   // the forced height as TM (or kWideHalfTail), 0 chosen per launch
 
 // workgroups of a 256-thread kernel one CU holds at once (looked up once per
 // kernel; at least 1)
@@ -805,35 +802,20 @@ constexpr int kWideLds = wide_rows(8) * (kWideN + 8) * 2;   // the staged TM = 8
 static_assert(kWideLds >= 2 * wide_stage(8) && kWideLds >= wide_rows(8) / 2 * (kWideN + 4) * 4,
               "LDS of the wide kernel");
 
-// the persistent tile loop of k_gemm_wide at tile height 32 TM
+// one tile of k_gemm_wide at tile height 32 TM: rows m0 .. m0 + 32 TM - 1,
+// columns n0 .. n0 + 255, K part z
 template <int TM, typename Epi>
-__device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __restrict__ A, int lda,
-                                           const uint16_t* __restrict__ W, float wscale, int M,
-                                           int N, int K, int m_cap, int splits,
-                                           float* __restrict__ part, const Epi& epi) {
+__device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __restrict__ A, int lda,
+                                          const uint16_t* __restrict__ W, float wscale, int M,
+                                          int N, int K, int m_cap, int splits,
+                                          float* __restrict__ part, const Epi& epi, int m0, int n0,
+                                          int z) {
     constexpr int TN = 4, WM = TM * 16, WN = TN * 16;
     constexpr int kRows = wide_rows(TM), kStage = wide_stage(TM) / 2;   // stage in elements
     constexpr int LPW = (kRows + kWideN) / 8 / 8;   // 16-byte loads per wavefront per stage
     static_assert(TM % 2 == 0 && TM >= 4 && TM <= 8, "tile heights of 128, 192 and 256 rows");
-
-    // Persistent: the grid has at most one workgroup per CU (G of them, a
-    // multiple of 8, dealt to the XCDs round-robin) and each loops over
-    // tiles. The tiles of the rows present this launch (M <= m_cap) are
-    // numbered in groups of kGroup row tiles, column-major inside a group; XCD
-    // x takes the x-th contiguous eighth of that order and its G / 8
-    // workgroups stride through it, so the concurrent tiles of an XCD share
-    // operand slices in its L2 and every XCD gets an equal share however few
-    // rows are present.
-    const int tiles_m = (M + kRows - 1) / kRows, tiles_n = N / kWideN;
-    const int total = tiles_m * tiles_n * splits;
-    const int per_xcd = (total + 7) >> 3;
-    const int xcd = (int)(blockIdx.x & 7), slot = (int)(blockIdx.x >> 3);
-    const int stride = (int)(gridDim.x >> 3);
-    const int lin_end = min((xcd + 1) * per_xcd, total);
     const int Ks = K / splits;
     const int nk = Ks / kWideK;
-    constexpr int kGroup = 4;
-
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int wm = wv >> 2, wn = wv & 3;
     const int lr = lane >> 3, lp = lane & 7;
@@ -854,162 +836,210 @@ __device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __res
         }
     }
 
-    for (int lin = xcd * per_xcd + slot; lin < lin_end; lin += stride) {
-        const int z = lin % splits, tl = lin / splits;
-        const int grp = tl / (kGroup * tiles_n), first = grp * kGroup;
-        const int gsz = min(tiles_m - first, kGroup);
-        const int in = tl - grp * kGroup * tiles_n;
-        const int tm = first + in % gsz, tn = in / gsz;
-        const int m0 = tm * kRows, n0 = tn * kWideN;
-        const int kbase = z * Ks;
+    const int kbase = z * Ks;
 
-        // wavefront wv loads 8-row blocks wv, wv + 8, ... of A then of W
-        const uint16_t* src[LPW];
+    // wavefront wv loads 8-row blocks wv, wv + 8, ... of A then of W
+    const uint16_t* src[LPW];
 #pragma unroll
-        for (int i = 0; i < LPW; ++i) {
-            const int f = wv + 8 * i;
-            const int r = 8 * (f < kRows / 8 ? f : f - kRows / 8) + lr;
-            const int c = (lp ^ (r & 7)) * 8;
-            src[i] = f < kRows / 8 ? A + (size_t)min(m0 + r, M - 1) * lda + kbase + c
-                                    : W + (size_t)(n0 + r) * K + kbase + c;
-        }
-        auto issue = [&](int kt, int st) {
-            kt = kt < nk ? kt : nk - 1;
-            uint16_t* sb = smem + st * kStage;
+    for (int i = 0; i < LPW; ++i) {
+        const int f = wv + 8 * i;
+        const int r = 8 * (f < kRows / 8 ? f : f - kRows / 8) + lr;
+        const int c = (lp ^ (r & 7)) * 8;
+        src[i] = f < kRows / 8 ? A + (size_t)min(m0 + r, M - 1) * lda + kbase + c
+                                : W + (size_t)(n0 + r) * K + kbase + c;
+    }
+    auto issue = [&](int kt, int st) {
+        kt = kt < nk ? kt : nk - 1;
+        uint16_t* sb = smem + st * kStage;
 #pragma unroll
-            for (int i = 0; i < LPW; ++i) load_to_lds16(src[i] + kt * kWideK, sb + (wv + 8 * i) * 512);
-        };
+        for (int i = 0; i < LPW; ++i) load_to_lds16(src[i] + kt * kWideK, sb + (wv + 8 * i) * 512);
+    };
 
-        f32x4_t acc[TM][TN];
+    f32x4_t acc[TM][TN];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-        __syncthreads();   // the previous tile's epilogue is done with LDS
-        issue(0, 0);
-        for (int kt = 0; kt < nk; ++kt) {
-            wait_loads<0>();
-            lds_barrier();
-            issue(kt + 1, (kt + 1) & 1);   // the last step re-reads its own tile into the idle stage
-            const uint16_t* sb = smem + (kt & 1) * kStage;
+    __syncthreads();   // the previous tile's epilogue is done with LDS
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_loads<0>();
+        lds_barrier();
+        issue(kt + 1, (kt + 1) & 1);   // the last step re-reads its own tile into the idle stage
+        const uint16_t* sb = smem + (kt & 1) * kStage;
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                f16x8_t a[TM], b[TN];
+        for (int h = 0; h < 2; ++h) {
+            f16x8_t a[TM], b[TN];
 #pragma unroll
-                for (int j = 0; j < TN; ++j) b[j] = *reinterpret_cast<const f16x8_t*>(sb + boff[h][j]);
+            for (int j = 0; j < TN; ++j) b[j] = *reinterpret_cast<const f16x8_t*>(sb + boff[h][j]);
 #pragma unroll
-                for (int i = 0; i < TM; ++i) a[i] = *reinterpret_cast<const f16x8_t*>(sb + aoff[h][i]);
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j],
-                                                                            0, 0, 0);
-            }
-            // Order of the step: the stage loads, six fragment reads, then
-            // four MFMAs (one a fragment times the four b) per further read,
-            // so each read has a group of MFMAs to hide behind instead of
-            // being waited for just before its own MFMAs (masks: 0x20 VMEM
-            // read, 0x100 DS read, 0x8 MFMA)
-            constexpr int kReads = 2 * (TM + TN), kGroups = 2 * TM;
-            __builtin_amdgcn_sched_group_barrier(0x020, LPW, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, kReads - kGroups + 2, 0);
-#pragma unroll
-            for (int g = 0; g < kGroups; ++g) {
-                __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-                if (g < kGroups - 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-        }
-        wait_loads<0>();   // the last (redundant) stage load has landed before LDS is reused
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] *= wscale;
-
-        const int col0 = n0 + wn * WN + (lane & 15);
-        if (part) {
-            float* P = part + (size_t)z * m_cap * N;
+            for (int i = 0; i < TM; ++i) a[i] = *reinterpret_cast<const f16x8_t*>(sb + aoff[h][i]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
-                    if (row >= M) continue;
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
-                }
-            continue;
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j],
+                                                                        0, 0, 0);
         }
-        Epi e = epi;
-        e.begin_tile(n0);
-        if constexpr (epi_stages_f32<Epi>(0)) {
-            // two passes of 16 TM rows (the wavefronts of one wm each) in fp32
-            constexpr int kLd = kWideN + 4;
-            float* ft = reinterpret_cast<float*>(smem);
+        // Order of the step: the stage loads, six fragment reads, then
+        // four MFMAs (one a fragment times the four b) per further read,
+        // so each read has a group of MFMAs to hide behind instead of
+        // being waited for just before its own MFMAs (masks: 0x20 VMEM
+        // read, 0x100 DS read, 0x8 MFMA)
+        constexpr int kReads = 2 * (TM + TN), kGroups = 2 * TM;
+        __builtin_amdgcn_sched_group_barrier(0x020, LPW, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, kReads - kGroups + 2, 0);
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                __syncthreads();   // operand stages, or the previous pass, are done with LDS
-                if (wm == half) {
-#pragma unroll
-                    for (int i = 0; i < TM; ++i)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-#pragma unroll
-                            for (int j = 0; j < TN; ++j)
-                                ft[(i * 16 + 4 * (lane >> 4) + v) * kLd + wn * WN + j * 16 + (lane & 15)] =
-                                    acc[i][j][v];
-                }
-                __syncthreads();
-                e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M);
-            }
-            continue;
-        } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
-            __syncthreads();   // every wavefront is done with the operand stages
-            const int ld = e.template tile_ld<kWideN>();
-            if constexpr (epi_stages_quads<Epi>(0)) {
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        e.stage_quad(smem, ld, wm * WM + i * 16 + 4 * (lane >> 4),
-                                     wn * WN + j * 16 + (lane & 15), acc[i][j]);
-            } else {
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int rl = wm * WM + i * 16 + 4 * (lane >> 4) + v;
-                    const typename Epi::Row ri = e.row_info(min(m0 + rl, M - 1));
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        const float val = acc[i][j][v];
-                        const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
-                            0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
-                        e.stage(smem, ld, rl, wn * WN + j * 16 + (lane & 15),
-                                e.aux(ri, col0 + j * 16), col0 + j * 16, val, partner);
-                    }
-                }
-            }
-            __syncthreads();
-            e.template store_tile<kWideN, kRows, 512>(smem, n0, m0, M);
-            continue;
+        for (int g = 0; g < kGroups; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
+            if (g < kGroups - 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
+    }
+    wait_loads<0>();   // the last (redundant) stage load has landed before LDS is reused
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] *= wscale;
+
+    const int col0 = n0 + wn * WN + (lane & 15);
+    if (part) {
+        float* P = part + (size_t)z * m_cap * N;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
-                const bool ok = row < M;
-                const typename Epi::Row ri = e.row_info(min(row, M - 1));
+                if (row >= M) continue;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) P[(size_t)row * N + col0 + j * 16] = acc[i][j][v];
+            }
+        return;
+    }
+    Epi e = epi;
+    e.begin_tile(n0);
+    if constexpr (epi_stages_f32<Epi>(0)) {
+        // two passes of 16 TM rows (the wavefronts of one wm each) in fp32
+        constexpr int kLd = kWideN + 4;
+        float* ft = reinterpret_cast<float*>(smem);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            __syncthreads();   // operand stages, or the previous pass, are done with LDS
+            if (wm == half) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j)
+                            ft[(i * 16 + 4 * (lane >> 4) + v) * kLd + wn * WN + j * 16 + (lane & 15)] =
+                                acc[i][j][v];
+            }
+            __syncthreads();
+            e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M);
+        }
+        return;
+    } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
+        __syncthreads();   // every wavefront is done with the operand stages
+        const int ld = e.template tile_ld<kWideN>();
+        if constexpr (epi_stages_quads<Epi>(0)) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    e.stage_quad(smem, ld, wm * WM + i * 16 + 4 * (lane >> 4),
+                                 wn * WN + j * 16 + (lane & 15), acc[i][j]);
+        } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int rl = wm * WM + i * 16 + 4 * (lane >> 4) + v;
+                const typename Epi::Row ri = e.row_info(min(m0 + rl, M - 1));
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const float val = acc[i][j][v];
                     const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
                         0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
-                    if (ok) e.store(ri, e.aux(ri, col0 + j * 16), row, col0 + j * 16, val, partner);
+                    e.stage(smem, ld, rl, wn * WN + j * 16 + (lane & 15),
+                            e.aux(ri, col0 + j * 16), col0 + j * 16, val, partner);
                 }
             }
+        }
+        __syncthreads();
+        e.template store_tile<kWideN, kRows, 512>(smem, n0, m0, M);
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = m0 + wm * WM + i * 16 + 4 * (lane >> 4) + v;
+            const bool ok = row < M;
+            const typename Epi::Row ri = e.row_info(min(row, M - 1));
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const float val = acc[i][j][v];
+                const float partner = __int_as_float(__builtin_amdgcn_update_dpp(
+                    0, __float_as_int(val), 0xB1, 0xF, 0xF, false));
+                if (ok) e.store(ri, e.aux(ri, col0 + j * 16), row, col0 + j * 16, val, partner);
+            }
+        }
+}
+
+// The persistent tile loop of k_gemm_wide at tile height 32 TM. The grid has
+// at most one workgroup per CU (G of them, a multiple of 8, dealt to the XCDs
+// round-robin) and each loops over tiles. The tiles of the rows present this
+// launch (M <= m_cap) are numbered in groups of kGroup row tiles, column-major
+// inside a group; XCD x takes the x-th contiguous eighth of that order and
+// its G / 8 workgroups stride through it, so the concurrent tiles of an XCD
+// share operand slices in its L2 and every XCD gets an equal share however
+// few rows are present. With half_tail (TM = 8), an XCD whose last round
+// would be at most half full runs that round's tiles as two 128-row halves
+// each, one per workgroup: the round then costs a 128-row tile instead of a
+// 256-row one.
+template <int TM, typename Epi>
+__device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __restrict__ A, int lda,
+                                           const uint16_t* __restrict__ W, float wscale, int M,
+                                           int N, int K, int m_cap, int splits,
+                                           float* __restrict__ part, const Epi& epi,
+                                           bool half_tail) {
+    constexpr int kRows = wide_rows(TM), kGroup = 4;
+    const int tiles_m = (M + kRows - 1) / kRows, tiles_n = N / kWideN;
+    const int total = tiles_m * tiles_n * splits;
+    const int per_xcd = (total + 7) >> 3;
+    const int xcd = (int)(blockIdx.x & 7), slot = (int)(blockIdx.x >> 3);
+    const int stride = (int)(gridDim.x >> 3);
+    const int lin0 = xcd * per_xcd, lin_end = min(lin0 + per_xcd, total);
+    // tile lin: K part, then groups of kGroup row tiles, column-major inside
+    auto at = [&](int lin, int& m0, int& n0, int& z) {
+        z = lin % splits;
+        const int tl = lin / splits;
+        const int grp = tl / (kGroup * tiles_n), first = grp * kGroup;
+        const int gsz = min(tiles_m - first, kGroup);
+        const int in = tl - grp * kGroup * tiles_n;
+        m0 = (first + in % gsz) * kRows;
+        n0 = (in / gsz) * kWideN;
+    };
+    const int count = max(lin_end - lin0, 0), full = count / stride, rest = count - full * stride;
+    const bool halves = TM == 8 && half_tail && rest > 0 && 2 * rest <= stride;
+    const int lin_stop = halves ? lin0 + full * stride : lin_end;
+    for (int lin = lin0 + slot; lin < lin_stop; lin += stride) {
+        int m0, n0, z;
+        at(lin, m0, n0, z);
+        wide_tile<TM>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z);
+    }
+    if constexpr (TM == 8) {
+        if (halves) {
+            const int lin = lin_stop + (slot >> 1);
+            if (lin < lin_end) {
+                int m0, n0, z;
+                at(lin, m0, n0, z);
+                m0 += wide_rows(4) * (slot & 1);
+                if (m0 < M)
+                    wide_tile<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z);
+            }
+        }
     }
 }
 
@@ -1030,11 +1060,11 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
     if (pick == 0) return;
     const int tm = force_tm ? force_tm : pick;
     if (tm == 4)
-        wide_tiles<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+        wide_tiles<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false);
     else if (tm == 6)
-        wide_tiles<6>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+        wide_tiles<6>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false);
     else
-        wide_tiles<8>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi);
+        wide_tiles<8>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, tm == kWideHalfTail);
 }
 
 // the wide kernel needs more than 64 KB of dynamic LDS: allowed once per
@@ -1300,7 +1330,8 @@ hipError_t gemm_setup() {
     g_force_tm = 0;
     if (f) {
         const struct { const char* name; int tile, tm; } opts[] = {
-            {"wide", 1, 0}, {"wide256", 1, 8}, {"wide192", 1, 6}, {"wide128", 1, 4}, {"small", -1, 0}};
+            {"wide", 1, 0},      {"wide256", 1, 8}, {"wide256h", 1, kWideHalfTail},
+            {"wide192", 1, 6},   {"wide128", 1, 4}, {"small", -1, 0}};
         for (const auto& o : opts)
             if (std::strcmp(f, o.name) == 0) {
                 g_force_tile = o.tile;
