@@ -292,14 +292,53 @@ def test_rollout_bf16_full_equals_compact_and_counts_are_bounded():
 
 @pytest.mark.parametrize("kernel", ["seq", "split"])
 def test_forward_bf16_each_attention_kernel_matches_oracle(kernel, monkeypatch):
-    """The two attention kernels (causal attention of each sequence's rows over
-    its own paged cache, Sec. 4.2): one wavefront walking a block's key tiles
-    in order, and four wavefronts splitting them and merging. A launch takes
-    one by its capacity; HBSJD_ATTN_KERNEL forces either on every launch. Both
+    """Two of the attention kernels (causal attention of each sequence's rows
+    over its own paged cache, Sec. 4.2): one wavefront walking a block's key
+    tiles in order, and four wavefronts splitting them and merging. A launch
+    takes one by its capacity; HBSJD_ATTN_KERNEL forces either on every
+    launch. Both
     meet the forward bar against the oracle on ragged prefill segments (1 to
     256 rows: one to eight 32-row query blocks)."""
     monkeypatch.setenv("HBSJD_ATTN_KERNEL", kernel)
     _bf16_forward_case("llamagen_b", [40, 0, 90, 255, 17], 11)
+
+
+def test_forward_bf16_query_split_attention_matches_oracle(monkeypatch):
+    """The attention kernel of the rounds (segments of at most 64 rows: four
+    wavefronts take 16 query rows each and share the key tiles through LDS),
+    forced on every launch it fits, meets the forward bar against the oracle
+    on ragged segments of 1 to 64 rows."""
+    monkeypatch.setenv("HBSJD_ATTN_KERNEL", "qs")
+    _bf16_forward_case("llamagen_b", [40, 0, 63, 16, 17, 5], 12)
+
+
+@pytest.mark.parametrize("W", [8, 16, 32, 63])
+def test_rollout_bf16_query_split_attention_equals_sequential(W, monkeypatch):
+    """The query-split attention kernel computes every row with the sequential
+    kernel's arithmetic, so a rollout forced onto it (every round; the
+    prefill's long segments take the sequential kernel) gives the
+    same tokens and counts as one forced onto the sequential kernel, in Full
+    and Compact rounds alike (Sec. 4.3), at windows of 9 to 64 rows."""
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 1, batch=8)
+    batch.prefix_len[3] = shape.T - 5
+    outs = {}
+    for kernel in ["seq", "qs"]:
+        monkeypatch.setenv("HBSJD_ATTN_KERNEL", kernel)
+        ctx = gu.make_ctx(shape, "bf16", blob)
+        for mode in [P().EXEC_FULL, P().EXEC_COMPACT]:
+            o = ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                                  batch.temperature, W, top_k=wl.top_k, seed=1000,
+                                  exec_mode=mode, gamma=4)
+            outs[kernel, mode] = (o["tokens"].cpu().numpy(), o["counts"].cpu().numpy())
+        del ctx
+    monkeypatch.delenv("HBSJD_ATTN_KERNEL", raising=False)
+    ref = outs["seq", P().EXEC_FULL]
+    for key, (tok, cnt) in outs.items():
+        assert np.array_equal(tok, ref[0]), key
+        assert np.array_equal(cnt, ref[1]), key
 
 
 @pytest.mark.parametrize("W", [8, 16, 32])
@@ -687,9 +726,9 @@ def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
     rounds (Sec. 4.3) process the same row in launches of different sizes, so
     the kernels must agree bit for bit. Forward logits of the same sequences
     with every launch forced onto one kernel (HBSJD_GEMM_TILE: the wide kernel
-    at its chosen tile height or at 256, 192 or 128 rows, or the small-tile
-    kernel) and chosen per launch must be identical, at a row count where the
-    choice varies."""
+    at its chosen tile height, at 256, 192 or 128 rows, or at 256 rows with a
+    last round of 128-row halves; or the small-tile kernel) and chosen per
+    launch must be identical, at a row count where the choice varies."""
     wl = synth.WORKLOADS[name]
     shape = wl.model
     blob = synth.make_weights(shape, 0, std=wl.weight_std, bias_std=wl.bias_std)
@@ -700,7 +739,7 @@ def test_gemm_kernel_choice_does_not_change_results(monkeypatch, name):
     toks = rng.integers(0, shape.vocab, size=(n, shape.T)).astype(np.int32)
     labels = rng.integers(0, shape.n_classes + 1, size=n).astype(np.int32)
     outs = {}
-    for force in ["wide", "wide256", "wide192", "wide128", "small", ""]:
+    for force in ["wide", "wide256", "wide256h", "wide192", "wide128", "small", ""]:
         if force:
             monkeypatch.setenv("HBSJD_GEMM_TILE", force)
         else:
