@@ -391,6 +391,156 @@ __global__ __launch_bounds__(64) void k_attn_f16_seq(const uint16_t* __restrict_
     }
 }
 
+// fp16, one workgroup of four wavefronts per (segment, head) for segments of
+// at most 64 rows: wavefront w takes query rows 16 w .. 16 w + 15, and all
+// four stream the segment's K and V^T tiles through two LDS buffers with
+// direct loads (global_load_lds_dwordx4), tile t + 1's loads issued while
+// tile t is multiplied. Prefetch then costs LDS instead of registers (87
+// VGPRs, five workgroups per CU), and each tile leaves memory once for every
+// query block. (Walking two or four heads per workgroup as one stream, so the
+// next head's first tile is in flight too, measured slower: fewer
+// workgroups.) Every wavefront walks the tiles up to the segment's last row,
+// as a 48-row block of k_attn_f16_seq does, with the same per-row arithmetic,
+// so rows come out bit-identical to it. LDS rows hold eight 16-byte chunks;
+// chunk c of row r sits at c ^ f(r), with f chosen so that the eight lanes of
+// a fragment read land on eight different chunk positions: K rows are read in
+// the permuted order of the score layout (rows 8a + b, b < 4, together),
+// f(r) = (r & 3) | ((r >> 1) & 4); V^T rows are read consecutively,
+// f(r) = r & 7.
+__device__ __forceinline__ int qs_swz_k(int r) { return (r & 3) | ((r >> 1) & 4); }
+__device__ __forceinline__ int qs_swz_v(int r) { return r & 7; }
+
+__global__ __launch_bounds__(256) void k_attn_f16_qs(const uint16_t* __restrict__ qb,
+                                                     uint16_t* __restrict__ ob, int d, int H,
+                                                     const uint16_t* __restrict__ kv, int maxp,
+                                                     Segments seg, const int* __restrict__ nseg_dev) {
+    // [buffer][K, V^T][64 rows x 64], 32 KB
+    __shared__ __attribute__((aligned(1024))) uint16_t kvs[2][2][64 * 64];
+    const int sg = blockIdx.x, head = blockIdx.y;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int nseg = *nseg_dev;
+    const int nrows = seg.nrows[sg];
+    const int row0s = seg.row0[sg];
+    const int pos0 = seg.pos0[sg];
+    const int pagev = seg.pages[(size_t)sg * maxp + min(lane, maxp - 1)];
+    if (sg >= nseg || nrows <= 0) return;   // the whole workgroup
+    const int ntiles = (pos0 + nrows - 1) / 64 + 1;
+    const int q0 = 16 * w;
+    const int nq = min(16, nrows - q0);   // <= 0: this wavefront only loads
+    const int posf = pos0 + q0;
+    const size_t page_elems = (size_t)2 * H * 64 * 64;
+
+    // wavefront w loads 1 KB blocks w, w + 4, w + 8, w + 12 of a tile (blocks
+    // 0-7 K rows, 8-15 V^T rows, 8 rows each): lane l's chunk lands at 16 l
+    // bytes into the block, LDS row 8 (b & 7) + (l >> 3), position l & 7
+    auto issue = [&](int tile, int buf) {
+        const int page = __builtin_amdgcn_readlane(pagev, tile);
+        const uint16_t* base = kv + (size_t)page * page_elems + (size_t)head * 4096;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int b = w + 4 * k;
+            const int part = b >> 3, r = 8 * (b & 7) + (lane >> 3);
+            const int c = (lane & 7) ^ (part == 0 ? qs_swz_k(r) : qs_swz_v(r));
+            const uint16_t* src = base + (size_t)part * H * 4096 + r * 64 + c * 8;
+            load_to_lds16(src, &kvs[buf][part][(b & 7) * 512]);
+        }
+    };
+    f16x8_t qf[2];
+    f32x4_t o[4];
+    float m = -INFINITY, l = 0.f;
+    if (nq > 0) {
+        const int rr = min(c16, nq - 1);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const f16x8_t x = load_f16x8(qb + (size_t)(row0s + q0 + rr) * d + head * 64 + kk * 32 + 8 * g);
+            qf[kk] = c16 < nq ? x : f16x8_t{};
+        }
+    }
+#pragma unroll
+    for (int dj = 0; dj < 4; ++dj) o[dj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int krow = 8 * (c16 >> 2) + (c16 & 3);
+    constexpr float kScale = 0.125f * 1.44269504088896340736f;
+
+    issue(0, 0);
+    for (int tile = 0; tile < ntiles; ++tile) {
+        wait_loads<0>();
+        lds_barrier();   // tile's loads landed everywhere; the other buffer is free
+        if (tile + 1 < ntiles) issue(tile + 1, (tile + 1) & 1);
+        if (nq <= 0) continue;
+        const uint16_t* Ks = kvs[tile & 1][0];
+        const uint16_t* Vs = kvs[tile & 1][1];
+        f32x4_t s[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const int r = 32 * (j >> 1) + 4 * (j & 1) + krow;
+#pragma unroll
+            for (int kd = 0; kd < 2; ++kd) {
+                const f16x8_t kf = load_f16x8(Ks + r * 64 + (((kd * 4 + g) ^ qs_swz_k(r)) << 3));
+                s[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[kd], s[j], 0, 0, 0);
+            }
+        }
+        // as in k_attn_f16_seq: element v of group j is key tile * 64 +
+        // 32 (j >> 1) + 8 g + 4 (j & 1) + v, visible while
+        // v <= lim - 32 (j >> 1) - 4 (j & 1)
+        const int lim = posf + c16 - tile * 64 - 8 * g;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float x = s[j][v] * kScale;
+                if (v > lim - 32 * (j >> 1) - 4 * (j & 1)) x = -INFINITY;
+                s[j][v] = x;
+                mx = fmaxf(mx, x);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float mnew = fmaxf(m, mx);
+        const float alpha = exp2f(m - mnew);
+        float ps = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float pv = exp2f(s[j][v] - mnew);
+                s[j][v] = pv;
+                ps += pv;
+            }
+        l = l * alpha + ps;
+        m = mnew;
+#pragma unroll
+        for (int dj = 0; dj < 4; ++dj) o[dj] *= alpha;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            f16x8_t pf;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                pf[e] = (_Float16)s[2 * kk][e];
+                pf[4 + e] = (_Float16)s[2 * kk + 1][e];
+            }
+#pragma unroll
+            for (int dj = 0; dj < 4; ++dj) {
+                const int r = dj * 16 + c16;
+                const f16x8_t vf = load_f16x8(Vs + r * 64 + (((kk * 4 + g) ^ qs_swz_v(r)) << 3));
+                o[dj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pf, o[dj], 0, 0, 0);
+            }
+        }
+    }
+    if (nq <= 0) return;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (c16 >= nq) return;
+    uint16_t* dst = ob + (size_t)(row0s + q0 + c16) * d + head * 64 + 4 * g;
+#pragma unroll
+    for (int dj = 0; dj < 4; ++dj) {
+        uint32_t w0 = f32_to_f16_rne(o[dj][0] / l) | ((uint32_t)f32_to_f16_rne(o[dj][1] / l) << 16);
+        uint32_t w1 = f32_to_f16_rne(o[dj][2] / l) | ((uint32_t)f32_to_f16_rne(o[dj][3] / l) << 16);
+        *reinterpret_cast<uint2*>(dst + dj * 16) = make_uint2(w0, w1);
+    }
+}
+
 // fp32: one wavefront per (row, head); scores over keys 0..pos in LDS.
 __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
                                                  float* __restrict__ o, int d, int H, int dh,
@@ -436,11 +586,13 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float* __restrict__ q,
     }
 }
 
-static int g_force_attn = 0;   // HBSJD_ATTN_KERNEL: 1 "seq", -1 "split", 0 chosen per launch
+// HBSJD_ATTN_KERNEL: 2 "qs" (else "seq"), 1 "seq", -1 "split", 0 chosen per launch
+static int g_force_attn = 0;
 
 void attention_setup() {
     const char* f = std::getenv("HBSJD_ATTN_KERNEL");
-    g_force_attn = !f ? 0 : std::strcmp(f, "seq") == 0 ? 1 : std::strcmp(f, "split") == 0 ? -1 : 0;
+    g_force_attn = !f ? 0 : std::strcmp(f, "qs") == 0 ? 2 : std::strcmp(f, "seq") == 0 ? 1
+                 : std::strcmp(f, "split") == 0 ? -1 : 0;
 }
 
 void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
@@ -449,17 +601,29 @@ void attention(bool f16, const void* q, void* o, int d, int heads, int head_dim,
                const int* nrows_dev, int nrows_cap, hipStream_t s) {
     if (f16) {
         if (nseg_cap <= 0) return;
-        // one wavefront per (segment, query block, head) once the launch has
-        // at least 2048 of them (8 per CU) and the page list fits a wavefront;
-        // below that, four wavefronts split each block's keys. The choice
-        // depends only on the launch's capacities, so Full and Compact rounds
-        // take the same kernel.
+        // Segments of at most 64 rows (every round) whose launch has at least
+        // 512 (segment, head) pairs take k_attn_f16_qs; longer segments (the
+        // prefill) take one wavefront per (segment, query block, head) once
+        // the launch has at least 2048 of them (8 per CU). Both need the page
+        // list to fit a wavefront. Below that, four wavefronts split each
+        // block's keys. The choice depends only on the launch's capacities, so
+        // Full and Compact rounds take the same kernel. (HBSJD_ATTN_KERNEL
+        // forces one kernel for every launch it fits, for tests; "qs" takes
+        // the sequential kernel where the query-split one does not fit.)
         const int rows_blk = max_rows_per_seg <= 16 ? 16 : max_rows_per_seg <= 32 ? 32
                            : max_rows_per_seg <= 48 ? 48 : 32;
         const int qbl = (max_rows_per_seg + rows_blk - 1) / rows_blk;
-        // (HBSJD_ATTN_KERNEL forces one kernel for every launch, for tests)
         const bool seq_ok = max_pages <= 64;
-        const bool take_seq = g_force_attn > 0 ? seq_ok
+        const bool qs_ok = seq_ok && max_rows_per_seg <= 64;
+        const bool take_qs = g_force_attn == 2 ? qs_ok
+                           : g_force_attn != 0 ? false
+                           : qs_ok && (long)nseg_cap * heads >= 512;
+        if (take_qs) {
+            launch(k_attn_f16_qs, dim3(nseg_cap, heads), dim3(256), 0, s, (const uint16_t*)q,
+                   (uint16_t*)o, d, heads, (const uint16_t*)kv_layer, max_pages, seg, nseg_dev);
+            return;
+        }
+        const bool take_seq = g_force_attn >= 1 ? seq_ok
                             : g_force_attn < 0 ? false
                             : (long)nseg_cap * qbl * heads >= 2048 && seq_ok;
         if (take_seq) {
