@@ -100,6 +100,8 @@ def test_kernel_class_names():
     assert bench.kernel_class(_ATTN) == ("attn", False)
     assert bench.kernel_class("void hbsjd::k_attn_f16_seq<3>(unsigned short const*, int)") == (
         "attn", False)
+    assert bench.kernel_class("hbsjd::k_attn_f16_qs(unsigned short const*, unsigned short*)") == (
+        "attn", False)
     assert bench.kernel_class("hbsjd::k_transform(hbsjd::TransformArgs)") == ("transform", False)
     assert bench.kernel_class("hbsjd::k_transform_rows_setup(int)")[0] is None
     assert bench.kernel_class("__amd_rocclr_copyBuffer")[0] is None
