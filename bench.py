@@ -206,7 +206,8 @@ def path_work(shape, prefix_len, counts, W, cfg, esz=2):
 
 # kernel class of a dispatch: the GEMM classes by their epilogue type
 _GEMM_EPI = (("EpiQkv", "qkv"), ("EpiSwiGLU", "w13"), ("EpiNone<0>", "oproj"),
-             ("EpiNone<1>", "w2"), ("EpiLogits", "lmhead"))
+             ("EpiNone<1>", "w2"), ("EpiResidual<0>", "oproj"), ("EpiResidual<1>", "w2"),
+             ("EpiLogits", "lmhead"))
 _KERNEL_CLASS = {"k_attn_f16": "attn", "k_attn_f16_seq": "attn", "k_attn_f16_qs": "attn",
                  "k_attn_f32": "attn",
                  "k_reduce_norm": "norm",

@@ -334,15 +334,22 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         // split-K applies to the MFMA path only; the fp32 path writes one partial
         const int so = bf ? split_for(r.nrows_cap, d, d) : 1;
         const int s2 = bf ? split_for(r.nrows_cap, d, f) : 1;
+        // with one K part the MFMA path adds O and W2 into the residual stream
+        // in their epilogues and the norm only reads it (the same additions)
         {
             Timed tm(c, HBSJD_K_OPROJ);
-            gemm_partial(bf, 0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev, r.nrows_cap,
-                         so, as<float>(c->part), s);
+            if (bf && so == 1)
+                gemm_residual(0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev, r.nrows_cap,
+                              as<float>(c->h), s);
+            else
+                gemm_partial(bf, 0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev,
+                             r.nrows_cap, so, as<float>(c->part), s);
         }
         {
             Timed tm(c, HBSJD_K_NORM);
-            reduce_residual_norm(bf, as<float>(c->part), so, r.nrows_cap, as<float>(c->h),
-                                 r.nrows_dev, c->g_ffn[l], c->m.rms_eps, d, c->hb.p, s);
+            reduce_residual_norm(bf, as<float>(c->part), bf && so == 1 ? 0 : so, r.nrows_cap,
+                                 as<float>(c->h), r.nrows_dev, c->g_ffn[l], c->m.rms_eps, d,
+                                 c->hb.p, s);
         }
         {
             Timed tm(c, HBSJD_K_W13);
@@ -351,15 +358,20 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         }
         {
             Timed tm(c, HBSJD_K_W2);
-            gemm_partial(bf, 1, c->act.p, f, c->w2[l], c->s_2[l], d, f, r.nrows_dev, r.nrows_cap,
-                         s2, as<float>(c->part), s);
+            if (bf && s2 == 1)
+                gemm_residual(1, c->act.p, f, c->w2[l], c->s_2[l], d, f, r.nrows_dev, r.nrows_cap,
+                              as<float>(c->h), s);
+            else
+                gemm_partial(bf, 1, c->act.p, f, c->w2[l], c->s_2[l], d, f, r.nrows_dev,
+                             r.nrows_cap, s2, as<float>(c->part), s);
         }
         {
             // the next layer's attention norm, or the final norm after the last layer
             Timed tm(c, HBSJD_K_NORM);
-            reduce_residual_norm(bf, as<float>(c->part), s2, r.nrows_cap, as<float>(c->h),
-                                 r.nrows_dev, l + 1 < c->L ? c->g_attn[l + 1] : c->g_out,
-                                 c->m.rms_eps, d, c->hb.p, s);
+            reduce_residual_norm(bf, as<float>(c->part), bf && s2 == 1 ? 0 : s2, r.nrows_cap,
+                                 as<float>(c->h), r.nrows_dev,
+                                 l + 1 < c->L ? c->g_attn[l + 1] : c->g_out, c->m.rms_eps, d,
+                                 c->hb.p, s);
         }
     }
 }

@@ -1285,6 +1285,33 @@ static void partial_tag(bool f16, const void* A, int lda, const void* W, float w
     }
 }
 
+// The residual stream h += A W^T (rows below the count), when the product has
+// one K part: each element is added to h once by the tile that owns it, the
+// same single fp32 addition the norm kernel makes with a one-part sum.
+template <int Tag>
+struct EpiResidual {
+    float* h;
+    int ld;
+    struct Row {};
+    struct Aux {};
+    __device__ void begin_tile(int) {}
+    __device__ Row row_info(int) const { return Row{}; }
+    __device__ Aux aux(const Row&, int) const { return Aux{}; }
+    __device__ void store(const Row&, const Aux&, int m, int n, float v, float) const {
+        float* p = h + (size_t)m * ld + n;
+        *p = *p + v;
+    }
+    PartialTag<Tag> tag;
+};
+
+void gemm_residual(int tag, const void* A, int lda, const void* W, float wscale, int N, int K,
+                   const int* m_dev, int m_cap, float* h, hipStream_t s) {
+    if (tag == 0)
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, EpiResidual<0>{h, N}, s);
+    else
+        dispatch_f16(A, lda, W, wscale, N, K, m_dev, m_cap, 1, nullptr, EpiResidual<1>{h, N}, s);
+}
+
 void gemm_partial(bool f16, int tag, const void* A, int lda, const void* W, float wscale, int N,
                   int K, const int* m_dev, int m_cap, int splits, float* part, hipStream_t s) {
     if (tag == 0)
@@ -1345,7 +1372,8 @@ hipError_t gemm_setup() {
         g_cus = cus;
     const hipError_t e[] = {wide_allow_lds<EpiQkv<uint16_t>>(), wide_allow_lds<EpiSwiGLU<uint16_t>>(),
                             wide_allow_lds<EpiLogits<true>>(), wide_allow_lds<EpiLogits<false>>(),
-                            wide_allow_lds<EpiNone<0>>(), wide_allow_lds<EpiNone<1>>()};
+                            wide_allow_lds<EpiNone<0>>(), wide_allow_lds<EpiNone<1>>(),
+                            wide_allow_lds<EpiResidual<0>>(), wide_allow_lds<EpiResidual<1>>()};
     for (hipError_t x : e)
         if (x != hipSuccess) return x;
     return hipSuccess;

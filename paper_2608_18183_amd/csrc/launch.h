@@ -90,6 +90,9 @@ void mfma_probe(int workgroups, int iters, float* sink, hipStream_t s);
 int split_for(int m_cap, int N, int K);
 void gemm_partial(bool f16, int tag, const void* A, int lda, const void* W, float wscale, int N,
                   int K, const int* m_dev, int m_cap, int splits, float* part, hipStream_t s);
+// MFMA path with one K part: h[m_cap][N] += A W^T in the epilogue (tag as above)
+void gemm_residual(int tag, const void* A, int lda, const void* W, float wscale, int N, int K,
+                   const int* m_dev, int m_cap, float* h, hipStream_t s);
 void gemm_swiglu(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
                  const int* m_dev, int m_cap, void* act, hipStream_t s);
 void gemm_logits(bool f16, const void* A, int lda, const void* W, float wscale, int N, int K,
@@ -109,7 +112,8 @@ void embed_norm(bool f16, const RowMeta& rows, const int* nrows_dev, int nrows_c
 void rmsnorm(bool f16, const float* h, const int32_t* src_idx, const int* nrows_dev,
              int nrows_cap, const float* gain, float eps, int d, void* hb, hipStream_t s);
 // h += sum over splits (in split order) of part[split][m_cap][d]; then
-// hb = RMSNorm(h) * gain (hb may be null)
+// hb = RMSNorm(h) * gain (hb may be null). With splits = 0 the sum is already
+// in h (gemm_residual) and only hb is written.
 void reduce_residual_norm(bool f16, const float* part, int splits, int m_cap, float* h,
                           const int* nrows_dev, const float* gain, float eps, int d, void* hb,
                           hipStream_t s);

@@ -328,16 +328,19 @@ __global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ pa
     // one phase of loads, issued with the row count: every split's partial,
     // the residual and the gain (rows below m_cap are always allocated; rows
     // at or past the count store nothing)
+    // (splits = 0: the projection has already added its sum into h)
     const int nrows = *nrows_dev;
     const int nv = d >> 2;
     float4 pz[kSplitMax][NV4], hv[NV4], gv[NV4];
 #pragma unroll
     for (int k = 0; k < NV4; ++k) {
         const int c = min(lane + 64 * k, nv - 1);
+        if (splits > 0) {
 #pragma unroll
-        for (int z = 0; z < kSplitMax; ++z) {
-            const int zz = min(z, splits - 1);
-            pz[z][k] = reinterpret_cast<const float4*>(part + ((size_t)zz * m_cap + r) * d)[c];
+            for (int z = 0; z < kSplitMax; ++z) {
+                const int zz = min(z, splits - 1);
+                pz[z][k] = reinterpret_cast<const float4*>(part + ((size_t)zz * m_cap + r) * d)[c];
+            }
         }
         hv[k] = reinterpret_cast<const float4*>(h + (size_t)r * d)[c];
         gv[k] = reinterpret_cast<const float4*>(g)[c];
@@ -348,16 +351,20 @@ __global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ pa
 #pragma unroll
     for (int k = 0; k < NV4; ++k) {
         const bool in = lane + 64 * k < nv;
-        float4 acc = pz[0][k];
+        if (splits > 0) {
+            float4 acc = pz[0][k];
 #pragma unroll
-        for (int z = 1; z < kSplitMax; ++z)
-            if (z < splits) {   // split order
-                acc.x += pz[z][k].x;
-                acc.y += pz[z][k].y;
-                acc.z += pz[z][k].z;
-                acc.w += pz[z][k].w;
-            }
-        x[k] = make_float4(hv[k].x + acc.x, hv[k].y + acc.y, hv[k].z + acc.z, hv[k].w + acc.w);
+            for (int z = 1; z < kSplitMax; ++z)
+                if (z < splits) {   // split order
+                    acc.x += pz[z][k].x;
+                    acc.y += pz[z][k].y;
+                    acc.z += pz[z][k].z;
+                    acc.w += pz[z][k].w;
+                }
+            x[k] = make_float4(hv[k].x + acc.x, hv[k].y + acc.y, hv[k].z + acc.z, hv[k].w + acc.w);
+        } else {
+            x[k] = hv[k];
+        }
         if (in) {
             ss = fmaf(x[k].x, x[k].x, ss);
             ss = fmaf(x[k].y, x[k].y, ss);
@@ -365,9 +372,11 @@ __global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ pa
             ss = fmaf(x[k].w, x[k].w, ss);
         }
     }
+    if (splits > 0) {
 #pragma unroll
-    for (int k = 0; k < NV4; ++k)
-        if (lane + 64 * k < nv) reinterpret_cast<float4*>(h + (size_t)r * d)[lane + 64 * k] = x[k];
+        for (int k = 0; k < NV4; ++k)
+            if (lane + 64 * k < nv) reinterpret_cast<float4*>(h + (size_t)r * d)[lane + 64 * k] = x[k];
+    }
     if (!hb) return;
     ss = wave_sum(ss);
     const float rn = 1.0f / sqrtf(ss / (float)d + eps);

@@ -97,6 +97,9 @@ def test_kernel_class_names():
     assert bench.kernel_class(_WIDE) == ("w13", True)
     assert bench.kernel_class(_SMALL) == ("w13", False)
     assert bench.kernel_class(_W2) == ("w2", False)
+    assert bench.kernel_class(_W2.replace("EpiNone<1>", "EpiResidual<1>")) == ("w2", False)
+    assert bench.kernel_class(_WIDE.replace("EpiSwiGLU<unsigned short>", "EpiResidual<0>")) == (
+        "oproj", True)
     assert bench.kernel_class(_ATTN) == ("attn", False)
     assert bench.kernel_class("void hbsjd::k_attn_f16_seq<3>(unsigned short const*, int)") == (
         "attn", False)
