@@ -334,28 +334,26 @@ void forward_layers(hbsjd_ctx* c, const FwdRows& r) {
         // split-K applies to the MFMA path only; the fp32 path writes one partial
         const int so = bf ? split_for(r.nrows_cap, d, d) : 1;
         const int s2 = bf ? split_for(r.nrows_cap, d, f) : 1;
-        // with one K part the MFMA path adds O and W2 into the residual stream
-        // in their epilogues and the norm only reads it (the same additions)
         {
             Timed tm(c, HBSJD_K_OPROJ);
-            if (bf && so == 1)
-                gemm_residual(0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev, r.nrows_cap,
-                              as<float>(c->h), s);
-            else
-                gemm_partial(bf, 0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev,
-                             r.nrows_cap, so, as<float>(c->part), s);
+            gemm_partial(bf, 0, c->ob.p, d, c->wo[l], c->s_o[l], d, d, r.nrows_dev, r.nrows_cap,
+                         so, as<float>(c->part), s);
         }
         {
             Timed tm(c, HBSJD_K_NORM);
-            reduce_residual_norm(bf, as<float>(c->part), bf && so == 1 ? 0 : so, r.nrows_cap,
-                                 as<float>(c->h), r.nrows_dev, c->g_ffn[l], c->m.rms_eps, d,
-                                 c->hb.p, s);
+            reduce_residual_norm(bf, as<float>(c->part), so, r.nrows_cap, as<float>(c->h),
+                                 r.nrows_dev, c->g_ffn[l], c->m.rms_eps, d, c->hb.p, s);
         }
         {
             Timed tm(c, HBSJD_K_W13);
             gemm_swiglu(bf, c->hb.p, d, c->w13[l], c->s_13[l], 2 * f, d, r.nrows_dev, r.nrows_cap,
                         c->act.p, s);
         }
+        // With one K part the MFMA path adds W2 into the residual stream in its
+        // epilogue and the norm only reads it (the same additions). O keeps
+        // the partial sum: its launch is a single short round of tiles, whose
+        // read-modify-write of the residual would sit exposed at its end
+        // (XL: 42 + 24 us for O and its norm against 57 + 11).
         {
             Timed tm(c, HBSJD_K_W2);
             if (bf && s2 == 1)
