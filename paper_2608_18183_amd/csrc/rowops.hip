@@ -325,11 +325,12 @@ __global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ pa
     constexpr int kSplitMax = 4;
     const int r = blockIdx.x, lane = threadIdx.x;
     if (r >= m_cap) return;
-    // one phase of loads, issued with the row count: every split's partial,
-    // the residual and the gain (rows below m_cap are always allocated; rows
-    // at or past the count store nothing)
-    // (splits = 0: the projection has already added its sum into h)
+    // the row count first: the grid covers the capacity, and rows at or past
+    // the count (most of them in the last rounds) load and store nothing.
+    // Then one phase of loads: every split's partial (splits = 0: the
+    // projection has already added its sum into h), the residual and the gain.
     const int nrows = *nrows_dev;
+    if (r >= nrows) return;
     const int nv = d >> 2;
     float4 pz[kSplitMax][NV4], hv[NV4], gv[NV4];
 #pragma unroll
@@ -345,7 +346,6 @@ __global__ __launch_bounds__(64) void k_reduce_norm(const float* __restrict__ pa
         hv[k] = reinterpret_cast<const float4*>(h + (size_t)r * d)[c];
         gv[k] = reinterpret_cast<const float4*>(g)[c];
     }
-    if (r >= nrows) return;
     float4 x[NV4];
     float ss = 0.f;
 #pragma unroll
