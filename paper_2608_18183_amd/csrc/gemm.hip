@@ -167,14 +167,16 @@ struct EpiQkv {
     }
     // The wide kernel's path: RH rows of a BT-column tile staged in LDS as fp32
     // sums before RoPE, tile[(r - rb) * ld + c] for tile rows rb .. rb + RH - 1,
-    // written by NT threads. q and K: each thread takes 8 consecutive columns
+    // written by NT threads; rows[i] is row_info of tile row i (the kernel
+    // fetches them while the tile's main loop runs). q and K: each thread takes 8 consecutive columns
     // (four pairs of one head) of a row, fetches their four cos and four sin
     // values as two 16-byte loads, turns the pairs and stores 16 bytes. V^T:
     // each thread a row (= cache slot) and a strided set of dimensions, in
     // groups of RH threads, as many groups as a power of two that fits in NT
     // (4 groups for RH = 128 or 96, 8 for 64).
     template <int BT, int RH, int NT>
-    __device__ void store_rows_f32(const float* tile, int ld, int n0, int m0, int rb, int M) const {
+    __device__ void store_rows_f32(const float* tile, int ld, int n0, int m0, int rb, int M,
+                                   const Row* rows) const {
         const int t = threadIdx.x;
         const int c0 = n0 - part * d;
         const int head = c0 >> 6;
@@ -186,7 +188,7 @@ struct EpiQkv {
                 const int qd = t + NT * h, r = qd / kChunks, col = (qd % kChunks) * 8;
                 const int m = m0 + rb + r;
                 if (m >= M) continue;
-                const Row ri = row_info(m);
+                const Row ri = rows[rb + r];
                 const float4 xa = *reinterpret_cast<const float4*>(tile + r * ld + col);
                 const float4 xb = *reinterpret_cast<const float4*>(tile + r * ld + col + 4);
                 const int pi = ri.p * (kDh >> 1) + (((c0 + col) & (kDh - 1)) >> 1);
@@ -210,7 +212,7 @@ struct EpiQkv {
             static_assert(BT % kGroups == 0, "V^T columns per thread");
             const int r = t % RH, m = m0 + rb + r;
             if (t < kGroups * RH && m < M) {
-                const Row ri = row_info(m);
+                const Row ri = rows[rb + r];
                 T* dst = kv + ri.off + head * 64 * 64;
 #pragma unroll 8
                 for (int k = 0; k < BT / kGroups; ++k) {
@@ -863,6 +865,21 @@ __device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __rest
 
     __syncthreads();   // the previous tile's epilogue is done with LDS
     issue(0, 0);
+    Epi e = epi;
+    e.begin_tile(n0);
+    // A staged-fp32 epilogue (QKV) gets each tile row's record (position and
+    // cache offset) now, into the 2 KB of LDS past its staging area: the
+    // loads complete with the first stage's, which the first step waits for
+    // anyway, instead of in a dependent chain after the main loop.
+    typename Epi::Row* rows_lds = nullptr;
+    if constexpr (epi_stages_f32<Epi>(0)) {
+        static_assert(wide_rows(8) * sizeof(typename Epi::Row) <=
+                          kWideLds - wide_rows(8) / 2 * (kWideN + 4) * 4,
+                      "row records past the staging area");
+        rows_lds = reinterpret_cast<typename Epi::Row*>(reinterpret_cast<char*>(smem) + kWideLds -
+                                                        wide_rows(8) * sizeof(typename Epi::Row));
+        if (t < kRows) rows_lds[t] = e.row_info(min(m0 + t, M - 1));
+    }
     for (int kt = 0; kt < nk; ++kt) {
         wait_loads<0>();
         lds_barrier();
@@ -916,8 +933,6 @@ __device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __rest
             }
         return;
     }
-    Epi e = epi;
-    e.begin_tile(n0);
     if constexpr (epi_stages_f32<Epi>(0)) {
         // two passes of 16 TM rows (the wavefronts of one wm each) in fp32
         constexpr int kLd = kWideN + 4;
@@ -936,7 +951,8 @@ __device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __rest
                                 acc[i][j][v];
             }
             __syncthreads();
-            e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M);
+            e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M,
+                                                              rows_lds);
         }
         return;
     } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
