@@ -165,6 +165,27 @@ struct EpiQkv {
             }
         }
     }
+    // The 2D RoPE factors depend only on a position's grid row (pairs below
+    // dh / 4) or column (the rest) and the pair, so for a G x G grid they fit
+    // in [cos, sin][row half, column half][G][dh / 4] floats, 16 G floats per
+    // quarter: 8 KB at G = 32. The wide kernel gathers them from the tables
+    // (entries 1 + g G and 1 + g, the same values) into LDS once per launch.
+    // Returns G, or 0 when the grid does not fit (the tables are read from
+    // memory then).
+    static constexpr int kRopeGridMax = 32;
+    __device__ int rope_grid() const {
+        const int g = (int)(sqrtf((float)T_) + 0.5f);
+        return kDh == 64 && g * g == T_ && g <= kRopeGridMax ? g : 0;
+    }
+    template <int NT>
+    __device__ void load_rope(float* lds, int G) const {
+        for (int k = threadIdx.x; k < 4 * G * 16; k += NT) {
+            const int sc = k / (2 * G * 16), rem = k - sc * 2 * G * 16;
+            const int hf = rem / (G * 16), g = (rem - hf * G * 16) >> 4, ii = k & 15;
+            const int src = (hf == 0 ? 1 + g * G : 1 + g) * 32 + hf * 16 + ii;
+            lds[k] = (sc == 0 ? rc : rs)[src];
+        }
+    }
     // The wide kernel's path: RH rows of a BT-column tile staged in LDS as fp32
     // sums before RoPE, tile[(r - rb) * ld + c] for tile rows rb .. rb + RH - 1,
     // written by NT threads; rows[i] is row_info of tile row i (the kernel
@@ -176,7 +197,7 @@ struct EpiQkv {
     // (4 groups for RH = 128 or 96, 8 for 64).
     template <int BT, int RH, int NT>
     __device__ void store_rows_f32(const float* tile, int ld, int n0, int m0, int rb, int M,
-                                   const Row* rows) const {
+                                   const Row* rows, const float* rope, int G) const {
         const int t = threadIdx.x;
         const int c0 = n0 - part * d;
         const int head = c0 >> 6;
@@ -191,9 +212,19 @@ struct EpiQkv {
                 const Row ri = rows[rb + r];
                 const float4 xa = *reinterpret_cast<const float4*>(tile + r * ld + col);
                 const float4 xb = *reinterpret_cast<const float4*>(tile + r * ld + col + 4);
-                const int pi = ri.p * (kDh >> 1) + (((c0 + col) & (kDh - 1)) >> 1);
-                const float4 cs = *reinterpret_cast<const float4*>(rc + pi);
-                const float4 sn = *reinterpret_cast<const float4*>(rs + pi);
+                const int i0 = ((c0 + col) & (kDh - 1)) >> 1;   // first of four pairs
+                float4 cs, sn;
+                if (G) {   // the grid coordinate of the pairs' half, from LDS
+                    const int hf = i0 >> 4, s1 = ri.p - 1;
+                    const int g = ri.p == 0 ? 0 : hf == 0 ? s1 / G : s1 - (s1 / G) * G;
+                    const float* f = rope + (hf * G + g) * 16 + (i0 & 15);
+                    cs = *reinterpret_cast<const float4*>(f);
+                    sn = *reinterpret_cast<const float4*>(f + 2 * G * 16);
+                } else {
+                    const int pi = ri.p * (kDh >> 1) + i0;
+                    cs = *reinterpret_cast<const float4*>(rc + pi);
+                    sn = *reinterpret_cast<const float4*>(rs + pi);
+                }
                 const float x[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
                 const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
                 u32x4_t out;
@@ -801,8 +832,12 @@ constexpr int kWideN = 256, kWideK = 64;
 constexpr int wide_rows(int tm) { return 32 * tm; }
 constexpr int wide_stage(int tm) { return (wide_rows(tm) + kWideN) * kWideK * 2; }   // bytes
 constexpr int kWideLds = wide_rows(8) * (kWideN + 8) * 2;   // the staged TM = 8 tile (> 2 stages)
+// past it, the QKV epilogue's RoPE tables (EpiQkv::load_rope, G <= 32)
+constexpr int kWideRopeLds = 4 * 32 * 16 * 4;
+constexpr int kWideLdsTotal = kWideLds + kWideRopeLds;
 static_assert(kWideLds >= 2 * wide_stage(8) && kWideLds >= wide_rows(8) / 2 * (kWideN + 4) * 4,
               "LDS of the wide kernel");
+static_assert(kWideLdsTotal <= 160 * 1024, "LDS of one CU");
 
 // one tile of k_gemm_wide at tile height 32 TM: rows m0 .. m0 + 32 TM - 1,
 // columns n0 .. n0 + 255, K part z
@@ -811,7 +846,7 @@ __device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __rest
                                           const uint16_t* __restrict__ W, float wscale, int M,
                                           int N, int K, int m_cap, int splits,
                                           float* __restrict__ part, const Epi& epi, int m0, int n0,
-                                          int z) {
+                                          int z, int rope_g) {
     constexpr int TN = 4, WM = TM * 16, WN = TN * 16;
     constexpr int kRows = wide_rows(TM), kStage = wide_stage(TM) / 2;   // stage in elements
     constexpr int LPW = (kRows + kWideN) / 8 / 8;   // 16-byte loads per wavefront per stage
@@ -951,8 +986,10 @@ __device__ __forceinline__ void wide_tile(uint16_t* smem, const uint16_t* __rest
                                 acc[i][j][v];
             }
             __syncthreads();
-            e.template store_rows_f32<kWideN, kRows / 2, 512>(ft, kLd, n0, m0, half * (kRows / 2), M,
-                                                              rows_lds);
+            e.template store_rows_f32<kWideN, kRows / 2, 512>(
+                ft, kLd, n0, m0, half * (kRows / 2), M, rows_lds,
+                reinterpret_cast<const float*>(reinterpret_cast<const char*>(smem) + kWideLds),
+                rope_g);
         }
         return;
     } else if constexpr (epi_stores_tile<Epi>(kWideN)) {
@@ -1019,7 +1056,7 @@ __device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __res
                                            const uint16_t* __restrict__ W, float wscale, int M,
                                            int N, int K, int m_cap, int splits,
                                            float* __restrict__ part, const Epi& epi,
-                                           bool half_tail) {
+                                           bool half_tail, int rope_g) {
     constexpr int kRows = wide_rows(TM), kGroup = 4;
     const int tiles_m = (M + kRows - 1) / kRows, tiles_n = N / kWideN;
     const int total = tiles_m * tiles_n * splits;
@@ -1043,7 +1080,8 @@ __device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __res
     for (int lin = lin0 + slot; lin < lin_stop; lin += stride) {
         int m0, n0, z;
         at(lin, m0, n0, z);
-        wide_tile<TM>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z);
+        wide_tile<TM>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z,
+                      rope_g);
     }
     if constexpr (TM == 8) {
         if (halves) {
@@ -1053,7 +1091,8 @@ __device__ __forceinline__ void wide_tiles(uint16_t* smem, const uint16_t* __res
                 at(lin, m0, n0, z);
                 m0 += wide_rows(4) * (slot & 1);
                 if (m0 < M)
-                    wide_tile<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z);
+                    wide_tile<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, m0, n0, z,
+                                 rope_g);
             }
         }
     }
@@ -1075,12 +1114,22 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
     const int pick = wide_pick(M, N, K, splits, pair_cus > 0 ? pair_cus : (int)gridDim.x, pair_cus > 0);
     if (pick == 0) return;
     const int tm = force_tm ? force_tm : pick;
+    // the QKV epilogue's RoPE tables, past the tile region (visible after the
+    // first tile's barrier)
+    int rope_g = 0;
+    if constexpr (epi_stages_f32<Epi>(0)) {
+        rope_g = epi.rope_grid();
+        if (rope_g)
+            epi.template load_rope<512>(
+                reinterpret_cast<float*>(reinterpret_cast<char*>(smem) + kWideLds), rope_g);
+    }
     if (tm == 4)
-        wide_tiles<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false);
+        wide_tiles<4>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false, rope_g);
     else if (tm == 6)
-        wide_tiles<6>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false);
+        wide_tiles<6>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, false, rope_g);
     else
-        wide_tiles<8>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi, tm == kWideHalfTail);
+        wide_tiles<8>(smem, A, lda, W, wscale, M, N, K, m_cap, splits, part, epi,
+                      tm == kWideHalfTail, rope_g);
 }
 
 // the wide kernel needs more than 64 KB of dynamic LDS: allowed once per
@@ -1088,7 +1137,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wide(const uint16_t* __restrict
 template <typename Epi>
 static hipError_t wide_allow_lds() {
     return hipFuncSetAttribute((const void*)k_gemm_wide<Epi>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, kWideLds);
+                               hipFuncAttributeMaxDynamicSharedMemorySize, kWideLdsTotal);
 }
 
 template <typename Epi>
@@ -1099,7 +1148,7 @@ static void launch_wide(const void* A, int lda, const void* W, float wscale, int
     const int tiles = ((m_cap + wide_rows(4) - 1) / wide_rows(4)) * (N / kWideN) * splits;
     const int cap = (g_cus / 8) * 8;
     const int grid = std::max(8, std::min(cap, ((tiles + 7) / 8) * 8));
-    launch(k_gemm_wide<Epi>, dim3(grid), dim3(512), (uint32_t)kWideLds, s, (const uint16_t*)A, lda,
+    launch(k_gemm_wide<Epi>, dim3(grid), dim3(512), (uint32_t)kWideLdsTotal, s, (const uint16_t*)A, lda,
            (const uint16_t*)W, wscale, N, K, m_dev, m_cap, splits, pair_cus, g_force_tm, part,
            epi);
 }
