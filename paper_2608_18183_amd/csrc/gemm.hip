@@ -1366,6 +1366,28 @@ struct EpiResidual {
         float* p = h + (size_t)m * ld + n;
         *p = *p + v;
     }
+    // The wide kernel stages its tile in LDS as fp32 rows and each thread
+    // updates 16 bytes of a row at a time (the same additions).
+    __device__ int rope_grid() const { return 0; }
+    template <int NT>
+    __device__ void load_rope(float*, int) const {}
+    template <int BT, int RH, int NT>
+    __device__ void store_rows_f32(const float* tile, int ld_t, int n0, int m0, int rb, int M,
+                                   const Row*, const float*, int) const {
+        constexpr int kQuads = BT / 4;
+        static_assert(RH * kQuads % NT == 0, "quads per thread");
+        const int t = threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < RH * kQuads / NT; ++k) {
+            const int qd = t + NT * k, r = qd / kQuads, c = (qd % kQuads) * 4;
+            const int m = m0 + rb + r;
+            if (m >= M) continue;
+            float4* p = reinterpret_cast<float4*>(h + (size_t)m * ld + n0 + c);
+            const float4 v = *reinterpret_cast<const float4*>(tile + r * ld_t + c);
+            const float4 x = *p;
+            *p = make_float4(x.x + v.x, x.y + v.y, x.z + v.z, x.w + v.w);
+        }
+    }
     PartialTag<Tag> tag;
 };
 
