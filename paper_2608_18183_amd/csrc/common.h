@@ -136,7 +136,7 @@ __device__ inline uint64_t meta_seed(const int32_t* meta) {
 
 // the three uniforms of image b at sequence position t: draft, accept, resample
 struct Uniforms { float draft, acc, res; };
-__device__ inline Uniforms uniforms_at(uint64_t seed, int b, int t) {
+__device__ __forceinline__ Uniforms uniforms_at(uint64_t seed, int b, int t) {
     const U4 o = philox4x32_10(seed, (uint32_t)b, (uint32_t)t, 0u, 0u);
     return Uniforms{unit_float(o.x), unit_float(o.y), unit_float(o.z)};
 }

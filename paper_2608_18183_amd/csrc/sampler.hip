@@ -511,8 +511,9 @@ __device__ inline int block_inv_cdf_regs(const float (&w)[kChunk], int V, float 
 // from the residual max(0, p - q), where q is the proposal row `qrow`, or a
 // point mass on z when qrow is null (a history draft); from p itself when the
 // residual is zero everywhere in fp32. All 256 threads must call it.
-__device__ int replacement_draw(const float* __restrict__ pr, const float* __restrict__ qrow,
-                                int z, int V, float u, float* stage, float* cp, int* res) {
+__device__ __forceinline__ int replacement_draw(const float* __restrict__ pr,
+                                                const float* __restrict__ qrow, int z, int V,
+                                                float u, float* stage, float* cp, int* res) {
     const int t = threadIdx.x;
     float w[kChunk];
     stage_load_row(pr, V, stage, [&](int k, float x) { w[k] = x; });
