@@ -99,6 +99,11 @@ struct hbsjd_ctx {
     int sync = 0; // batch-synchronous windows instead of independent progress
     hipEvent_t ev_done = nullptr;   // teacher scoring: this context's forward has been queued
     int max_rounds = 0, max_pages = 0, rounds_launched = 0;
+    // an upper bound, known on the host, of the images active in the next
+    // round (images only ever finish, so a count read a round or two behind
+    // bounds it); sizes the kernel choice of the round's products
+    int a_bound = 0;
+    bool capturing = false;   // a round is being captured into a graph
     float cfg_scale = 0.f;
     uint64_t seed = 0;
     int32_t* counts = nullptr;   // device [max_rounds][B]
@@ -498,6 +503,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     HIPTRY(c, hipStreamWaitEvent(c->stream, c->ev_user, 0));
     c->max_rounds = a->max_rounds;
     c->rounds_launched = 0;
+    c->a_bound = B;
     const int cfg = c->cfg;
     const int S = B * cfg;
 
@@ -670,10 +676,27 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
     return HBSJD_OK;
 }
 
+// An upper bound of the next round's rows: every slot when the round can run
+// Full, else the rows of at most a_bound active images. A captured round
+// serves every round, so it takes none.
+int round_row_bound(const hbsjd_ctx* c) {
+    if (c->capturing) return -1;
+    const bool full = c->exec_mode == HBSJD_EXEC_FULL ||
+                      (c->exec_mode == HBSJD_EXEC_AUTO && c->a_bound > c->gamma);
+    return (full ? c->B : std::min(c->a_bound, c->B)) * c->cfg * (c->W + 1);
+}
+
+// the products of the calling thread take a row bound until the end of scope
+struct RowBound {
+    explicit RowBound(int rows) { gemm_row_bound(rows); }
+    ~RowBound() { gemm_row_bound(-1); }
+};
+
 // queue the launches of one round on buffer parity `cur`; every launch sizes
 // itself from the device counts the round's set-up kernel writes
 void enqueue_round(hbsjd_ctx* c, int cur, bool with_verify = true) {
     hipStream_t s = c->stream;
+    RowBound rb(round_row_bound(c));
     const int B = c->B, W = c->W, cfg = c->cfg, S = B * cfg, R = W + 1;
     int32_t* mt = as<int32_t>(c->meta);
     RoundSetupArgs sa{B, W, c->T, cfg, c->C, c->max_pages, c->max_rounds,
@@ -756,7 +779,9 @@ hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
     for (int par = 0; par < 2; ++par) {
         hipGraph_t graph = nullptr;
         HIPTRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
+        c->capturing = true;
         enqueue_round(c, par);
+        c->capturing = false;
         hipError_t e = hipStreamEndCapture(c->stream, &graph);
         if (e != hipSuccess) return hip_fail(c, e, "hipStreamEndCapture");
         e = hipGraphInstantiate(&c->gexec[par], graph, nullptr, nullptr, 0);
@@ -1094,6 +1119,7 @@ hbsjd_status hbsjd_rollout(hbsjd_ctx* c, const hbsjd_rollout_args* a, hbsjd_roll
                     rounds = r - 1;
                     break;
                 }
+                c->a_bound = std::min(c->a_bound, (int)c->pin[(r - 1) & 1]);
             }
         }
         HIPTRY(c, hipMemcpyAsync(o->tokens, c->xtok.p, (size_t)c->B * c->T * 4,
@@ -1151,11 +1177,10 @@ hbsjd_status hbsjd_round(hbsjd_ctx* c, int32_t exec_mode, int32_t* counts, int32
         HIPTRY(c, hipMemcpyAsync(cur.data(), c->cursor.p, c->B * 4, hipMemcpyDeviceToHost, c->stream));
         HIPTRY(c, hipStreamSynchronize(c->stream));
         TRY(check_device_error(c));
-        if (active) {
-            int n = 0;
-            for (int b = 0; b < c->B; ++b) n += cur[b] < c->T;
-            *active = n;
-        }
+        int n = 0;
+        for (int b = 0; b < c->B; ++b) n += cur[b] < c->T;
+        c->a_bound = n;
+        if (active) *active = n;
         return HBSJD_OK;
     } catch (...) {
         return fail(HBSJD_EINTERNAL, "unexpected host exception in hbsjd_round");
@@ -1545,6 +1570,7 @@ hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* c, int32_t batch, int32_t window, 
         HIPTRY(c, hipEventCreate(&e0));
         HIPTRY(c, hipEventCreate(&e1));
         auto time_mode = [&](int exec, float* us) -> hbsjd_status {
+            c->exec_mode = exec;           // with a_bound, the row bound of the timed rounds
             int32_t hdr[2] = {-1, exec};   // round index, exec mode
             HIPTRY(c, hipMemcpyAsync(as<int32_t>(c->meta) + kMetaRound, &hdr[0], 4, hipMemcpyHostToDevice, s));
             HIPTRY(c, hipMemcpyAsync(as<int32_t>(c->meta) + kMetaExec, &hdr[1], 4, hipMemcpyHostToDevice, s));
@@ -1574,6 +1600,7 @@ hbsjd_status hbsjd_calibrate_gamma(hbsjd_ctx* c, int32_t batch, int32_t window, 
             }
             for (int b = 0; b < B; ++b) cur[b] = b < A ? k : T;
             HIPTRY(c, hipMemcpyAsync(c->cursor.p, cur.data(), B * 4, hipMemcpyHostToDevice, s));
+            c->a_bound = A;
             float t_full = 0.f, t_compact = 0.f;
             if ((st = time_mode(HBSJD_EXEC_FULL, &t_full)) != HBSJD_OK) break;
             if ((st = time_mode(HBSJD_EXEC_COMPACT, &t_compact)) != HBSJD_OK) break;

@@ -1193,8 +1193,12 @@ static void launch_f16(const void* A, int lda, const void* W, float wscale, int 
 // the row count and wide_pick tells which one works. (A persistent launch
 // that finds no work costs a few microseconds; a wide-tile launch sized for
 // the capacity would cost its idle workgroups' dispatch, about as much as
-// the work of a full launch.)
+// the work of a full launch.) With a host-side bound on the rows
+// (gemm_row_bound) only the kernel wide_pick picks for the bound is launched.
 constexpr int kWideMin = 96;   // capacity in 256 x 256 tiles below which it is not tried
+
+static thread_local int g_row_bound = -1;
+void gemm_row_bound(int rows) { g_row_bound = rows; }
 
 template <typename Epi>
 static void dispatch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
@@ -1214,13 +1218,14 @@ static void dispatch_f16(const void* A, int lda, const void* W, float wscale, in
         return;
     }
     const bool wide = fit && t256 >= kWideMin;
-    if (wide && !m_dev) {   // the rows are known here: the same choice on the host
-        if (wide_pick(m_cap, N, K, splits, g_cus, true) != 0) {
+    // rows known on the host, exactly (no device count) or as an upper bound:
+    // the kernel wide_pick picks for that many rows, alone
+    const int m_host = !m_dev ? m_cap : g_row_bound >= 0 ? std::max(1, std::min(g_row_bound, m_cap)) : 0;
+    if (m_host > 0) {
+        if (wide && wide_pick(m_host, N, K, splits, g_cus, true) != 0) {
             launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
             return;
         }
-    }
-    if (!m_dev) {
         if (N % 128 == 0 && t128 >= 512)
             launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
         else

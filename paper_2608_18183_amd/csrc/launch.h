@@ -81,6 +81,13 @@ void gemm_qkv(bool f16, const void* A, int lda, const void* W, float wscale, int
               const int* m_dev, int m_cap, const QkvArgs& e, hipStream_t s);
 // once per process before any launch (the wide GEMM's LDS allowance)
 hipError_t gemm_setup();
+// An upper bound, known on the host, of the rows present in this thread's
+// following launches whose row count is read on the device (-1: none). With
+// one, such a product launches the single kernel that suits the bound instead
+// of two kernels that choose between themselves on the device. Any kernel is
+// correct for any row count up to the launch's cap, so a bound that is too
+// small only costs speed.
+void gemm_row_bound(int rows);
 // reads HBSJD_ATTN_KERNEL ("seq" / "split": one attention kernel for every launch)
 void attention_setup();
 // MFMA calibration kernel: workgroups x 4 wavefronts x iters x 8 MFMAs (16384 flops each)
