@@ -103,15 +103,20 @@ struct hbsjd_ctx {
     // round (images only ever finish, so a count read a round or two behind
     // bounds it); sizes the kernel choice of the round's products
     int a_bound = 0;
-    bool capturing = false;   // a round is being captured into a graph
     float cfg_scale = 0.f;
     uint64_t seed = 0;
     int32_t* counts = nullptr;   // device [max_rounds][B]
     long kv_layer_elems = 0;
 
-    // the round as two captured graphs (buffer parity 0 and 1), valid while the
-    // launch arguments they bake in stay the same
-    hipGraphExec_t gexec[2] = {nullptr, nullptr};
+    // Captured rounds: each a pair of graphs (buffer parity 0 and 1) with the
+    // kernels its products were captured with. They are valid while the
+    // launch arguments they bake in stay the same (gsig); a pair serves a
+    // round whose row bound gives each of its products the same kernels.
+    struct RoundGraphs {
+        std::vector<GemmPlan> plan;
+        hipGraphExec_t exec[2] = {nullptr, nullptr};
+    };
+    std::vector<RoundGraphs> graphs;
     std::vector<uint64_t> gsig;
     bool use_graphs = true;
 
@@ -193,8 +198,9 @@ hbsjd_ctx::~hbsjd_ctx() {
         (void)hipEventDestroy(pr.second.second);
     }
     for (hipEvent_t e : prof_free) (void)hipEventDestroy(e);
-    for (auto& g : gexec)
-        if (g) (void)hipGraphExecDestroy(g);
+    for (auto& g : graphs)
+        for (hipGraphExec_t e : g.exec)
+            if (e) (void)hipGraphExecDestroy(e);
     if (ev_user) (void)hipEventDestroy(ev_user);
     if (ev_done) (void)hipEventDestroy(ev_done);
     if (stream) (void)hipStreamDestroy(stream);
@@ -677,10 +683,8 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
 }
 
 // An upper bound of the next round's rows: every slot when the round can run
-// Full, else the rows of at most a_bound active images. A captured round
-// serves every round, so it takes none.
+// Full, else the rows of at most a_bound active images.
 int round_row_bound(const hbsjd_ctx* c) {
-    if (c->capturing) return -1;
     const bool full = c->exec_mode == HBSJD_EXEC_FULL ||
                       (c->exec_mode == HBSJD_EXEC_AUTO && c->a_bound > c->gamma);
     return (full ? c->B : std::min(c->a_bound, c->B)) * c->cfg * (c->W + 1);
@@ -769,26 +773,54 @@ std::vector<uint64_t> graph_signature(hbsjd_ctx* c) {
     return g;
 }
 
-hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
-    for (auto& g : c->gexec)
-        if (g) {
-            HIPTRY(c, hipGraphExecDestroy(g));
-            g = nullptr;
-        }
+void drop_round_graphs(hbsjd_ctx* c) {
+    for (auto& g : c->graphs)
+        for (hipGraphExec_t e : g.exec)
+            if (e) (void)hipGraphExecDestroy(e);
+    c->graphs.clear();
     c->gsig.clear();
+}
+
+// the products' kernels for a row bound match those a pair was captured with
+bool plan_holds(const std::vector<GemmPlan>& plan, int row_bound) {
+    for (const GemmPlan& p : plan)
+        if (gemm_plan(p, row_bound) != p.kernels) return false;
+    return true;
+}
+
+// while alive, the calling thread's products record their kernels in `log`
+struct PlanLog {
+    explicit PlanLog(std::vector<GemmPlan>* log) { gemm_plan_log(log); }
+    ~PlanLog() { gemm_plan_log(nullptr); }
+};
+
+// capture the round, under the current row bound, as one more pair of graphs
+// (the pairs of other bounds are kept, up to kMaxRoundGraphs)
+constexpr size_t kMaxRoundGraphs = 8;
+hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
+    if (c->graphs.size() >= kMaxRoundGraphs) drop_round_graphs(c);
+    hbsjd_ctx::RoundGraphs g;
     for (int par = 0; par < 2; ++par) {
         hipGraph_t graph = nullptr;
-        HIPTRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
-        c->capturing = true;
-        enqueue_round(c, par);
-        c->capturing = false;
-        hipError_t e = hipStreamEndCapture(c->stream, &graph);
-        if (e != hipSuccess) return hip_fail(c, e, "hipStreamEndCapture");
-        e = hipGraphInstantiate(&c->gexec[par], graph, nullptr, nullptr, 0);
-        (void)hipGraphDestroy(graph);
-        if (e != hipSuccess) return hip_fail(c, e, "hipGraphInstantiate");
+        std::vector<GemmPlan> log;
+        hipError_t e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
+        if (e == hipSuccess) {
+            PlanLog pl(&log);
+            enqueue_round(c, par);
+            e = hipStreamEndCapture(c->stream, &graph);
+        }
+        if (e == hipSuccess) {
+            e = hipGraphInstantiate(&g.exec[par], graph, nullptr, nullptr, 0);
+            (void)hipGraphDestroy(graph);
+        }
+        if (e != hipSuccess) {
+            for (hipGraphExec_t x : g.exec)
+                if (x) (void)hipGraphExecDestroy(x);
+            return hip_fail(c, e, "round graph capture");
+        }
+        if (par == 0) g.plan = std::move(log);
     }
-    c->gsig = graph_signature(c);
+    c->graphs.push_back(std::move(g));
     return HBSJD_OK;
 }
 
@@ -796,8 +828,23 @@ hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
 hbsjd_status launch_round(hbsjd_ctx* c) {
     const int cur = c->rounds_launched & 1;
     if (c->use_graphs && c->prof_mask == 0) {
-        if (c->gsig != graph_signature(c)) TRY(capture_round_graphs(c));
-        HIPTRY(c, hipGraphLaunch(c->gexec[cur], c->stream));
+        std::vector<uint64_t> sig = graph_signature(c);
+        if (c->gsig != sig) {
+            drop_round_graphs(c);
+            c->gsig = std::move(sig);
+        }
+        const int bound = round_row_bound(c);
+        hbsjd_ctx::RoundGraphs* g = nullptr;
+        for (auto& x : c->graphs)
+            if (plan_holds(x.plan, bound)) {
+                g = &x;
+                break;
+            }
+        if (!g) {
+            TRY(capture_round_graphs(c));
+            g = &c->graphs.back();
+        }
+        HIPTRY(c, hipGraphLaunch(g->exec[cur], c->stream));
     } else {
         enqueue_round(c, cur);
         HIPTRY(c, hipGetLastError());

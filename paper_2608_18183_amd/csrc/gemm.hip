@@ -1198,45 +1198,45 @@ static void launch_f16(const void* A, int lda, const void* W, float wscale, int 
 constexpr int kWideMin = 96;   // capacity in 256 x 256 tiles below which it is not tried
 
 static thread_local int g_row_bound = -1;
+static thread_local std::vector<GemmPlan>* g_plan_log = nullptr;
 void gemm_row_bound(int rows) { g_row_bound = rows; }
+void gemm_plan_log(std::vector<GemmPlan>* log) { g_plan_log = log; }
+
+// the kernels of a product of N x K weights over up to m_cap rows (m_dev: the
+// row count is read on the device), under the calling thread's row bound
+static int plan_kernels(int N, int K, bool m_dev, int m_cap, int splits, bool wide_ok,
+                        int row_bound) {
+    const long t256 = (long)((m_cap + 255) / 256) * (N / 256) * splits;
+    const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
+    const bool fit = wide_ok && N % 256 == 0 && (K / splits) % kWideK == 0;
+    const int small = N % 128 == 0 && t128 >= 512 ? kGemm128 : kGemm64;
+    if (g_force_tile != 0)   // HBSJD_GEMM_TILE: one kernel for every launch (results are the same)
+        return g_force_tile > 0 && fit ? kGemmWide : small;
+    const bool wide = fit && t256 >= kWideMin;
+    // rows known on the host, exactly (no device count) or as an upper bound:
+    // the kernel wide_pick picks for that many rows, alone
+    const int m_host = !m_dev ? m_cap : row_bound >= 0 ? std::max(1, std::min(row_bound, m_cap)) : 0;
+    if (m_host > 0) return wide && wide_pick(m_host, N, K, splits, g_cus, true) != 0 ? kGemmWide : small;
+    return wide ? small | kGemmPair : small;
+}
+
+int gemm_plan(const GemmPlan& p, int row_bound) {
+    return plan_kernels(p.N, p.K, true, p.m_cap, p.splits, p.wide_ok, row_bound);
+}
 
 template <typename Epi>
 static void dispatch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
                          const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
                          hipStream_t s, bool wide_ok = true) {
-    const long t256 = (long)((m_cap + 255) / 256) * (N / 256) * splits;
-    const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
-    const bool fit = wide_ok && N % 256 == 0 && (K / splits) % kWideK == 0;
-    if (g_force_tile != 0) {   // HBSJD_GEMM_TILE: one kernel for every launch (results are the same)
-        if (g_force_tile > 0 && fit) {
-            launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
-        } else if (N % 128 == 0 && t128 >= 512) {
-            launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
-        } else {
-            launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
-        }
-        return;
-    }
-    const bool wide = fit && t256 >= kWideMin;
-    // rows known on the host, exactly (no device count) or as an upper bound:
-    // the kernel wide_pick picks for that many rows, alone
-    const int m_host = !m_dev ? m_cap : g_row_bound >= 0 ? std::max(1, std::min(g_row_bound, m_cap)) : 0;
-    if (m_host > 0) {
-        if (wide && wide_pick(m_host, N, K, splits, g_cus, true) != 0) {
-            launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, 0, part, epi, s);
-            return;
-        }
-        if (N % 128 == 0 && t128 >= 512)
-            launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
-        else
-            launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s);
-        return;
-    }
-    const int pair = wide ? g_cus : 0;
-    if (wide) launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, pair, part, epi, s);
-    if (N % 128 == 0 && t128 >= 512)
+    const int k = plan_kernels(N, K, m_dev != nullptr, m_cap, splits, wide_ok, g_row_bound);
+    if (g_plan_log && m_dev) g_plan_log->push_back(GemmPlan{N, K, m_cap, splits, wide_ok, k});
+    // a pair: both kernels, each reads the row count and wide_pick tells which one works
+    const int pair = k & kGemmPair ? g_cus : 0;
+    if (k & (kGemmWide | kGemmPair))
+        launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, pair, part, epi, s);
+    if ((k & 3) == kGemm128)
         launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
-    else
+    else if ((k & 3) == kGemm64)
         launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
 }
 

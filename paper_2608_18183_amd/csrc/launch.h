@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <vector>
 
 #include "common.h"
 
@@ -88,6 +89,19 @@ hipError_t gemm_setup();
 // correct for any row count up to the launch's cap, so a bound that is too
 // small only costs speed.
 void gemm_row_bound(int rows);
+// The kernels of one product (kGemmWide alone, kGemm128 or kGemm64 alone, or
+// kGemmPair | the smaller-tile kernel), recorded with its shape by every
+// product with a device row count while a log is set (null: none). A captured
+// round is valid for another row bound while gemm_plan() gives every product
+// it recorded the same kernels under that bound.
+enum { kGemmWide = 4, kGemm128 = 1, kGemm64 = 2, kGemmPair = 8 };
+struct GemmPlan {
+    int N, K, m_cap, splits;
+    bool wide_ok;
+    int kernels;
+};
+void gemm_plan_log(std::vector<GemmPlan>* log);
+int gemm_plan(const GemmPlan& p, int row_bound);
 // reads HBSJD_ATTN_KERNEL ("seq" / "split": one attention kernel for every launch)
 void attention_setup();
 // MFMA calibration kernel: workgroups x 4 wavefronts x iters x 8 MFMAs (16384 flops each)

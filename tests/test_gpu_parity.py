@@ -584,11 +584,12 @@ def test_round_state_equals_oracle_windows(tiny, name):
 
 
 def test_graph_replays_equal_eager_launches(monkeypatch):
-    """Rounds run as two captured HIP graphs replayed every round (and across
-    rollouts); a context created with HBSJD_NO_GRAPHS=1 launches the same
-    kernels eagerly. Several rollouts, alternated between the two contexts so
-    eager work and synchronisations sit between the replays, must agree bit for
-    bit in tokens and per-round counts."""
+    """Rounds run as captured HIP graphs replayed every round (and across
+    rollouts), one pair per kernel plan of the round's products; a context
+    created with HBSJD_NO_GRAPHS=1 launches the same kernels eagerly. Several
+    rollouts, alternated between the two contexts so eager work and
+    synchronisations sit between the replays, must agree bit for bit in tokens
+    and per-round counts."""
     wl = synth.WORKLOADS["llamagen_b"]
     shape = wl.model
     blob = synth.make_weights(shape, 0)
@@ -608,6 +609,30 @@ def test_graph_replays_equal_eager_launches(monkeypatch):
         assert np.array_equal(outs[0]["tokens"].cpu().numpy(), outs[1]["tokens"].cpu().numpy())
         assert np.array_equal(outs[0]["counts"].cpu().numpy(), outs[1]["counts"].cpu().numpy())
         assert outs[0]["rounds"] == outs[1]["rounds"] and outs[0]["rounds"] > 2
+
+
+def test_graph_replays_follow_the_row_bound(monkeypatch):
+    """With 192 images of the B model a full round has 3264 rows, enough for
+    the wide GEMM kernel, and the products switch to smaller tiles as images
+    finish (prefix lengths spread over the grid), so the graph context
+    captures a pair per kernel plan while the eager one picks per round.
+    Tokens and counts must agree bit for bit."""
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 5, batch=192)
+    batch.prefix_len[:] = np.linspace(0, shape.T - 2, 192).astype(batch.prefix_len.dtype)
+    graph = gu.make_ctx(shape, "bf16", blob)
+    monkeypatch.setenv("HBSJD_NO_GRAPHS", "1")
+    eager = gu.make_ctx(shape, "bf16", blob)
+    monkeypatch.delenv("HBSJD_NO_GRAPHS")
+    for seed, mode in [(1000, P().EXEC_COMPACT), (1001, P().EXEC_AUTO)]:
+        outs = [c.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                                batch.temperature, wl.window, top_k=wl.top_k, seed=seed,
+                                exec_mode=mode, gamma=96) for c in (graph, eager)]
+        assert np.array_equal(outs[0]["tokens"].cpu().numpy(), outs[1]["tokens"].cpu().numpy())
+        assert np.array_equal(outs[0]["counts"].cpu().numpy(), outs[1]["counts"].cpu().numpy())
+        assert outs[0]["rounds"] == outs[1]["rounds"] and outs[0]["rounds"] > 10
 
 
 def test_argument_errors(tiny):
