@@ -114,6 +114,7 @@ struct hbsjd_ctx {
     // round whose row bound gives each of its products the same kernels.
     struct RoundGraphs {
         std::vector<GemmPlan> plan;
+        int bound = 0;   // the row bound it was captured under
         hipGraphExec_t exec[2] = {nullptr, nullptr};
     };
     std::vector<RoundGraphs> graphs;
@@ -820,6 +821,7 @@ hbsjd_status capture_round_graphs(hbsjd_ctx* c) {
         }
         if (par == 0) g.plan = std::move(log);
     }
+    g.bound = round_row_bound(c);
     c->graphs.push_back(std::move(g));
     return HBSJD_OK;
 }
@@ -836,7 +838,7 @@ hbsjd_status launch_round(hbsjd_ctx* c) {
         const int bound = round_row_bound(c);
         hbsjd_ctx::RoundGraphs* g = nullptr;
         for (auto& x : c->graphs)
-            if (plan_holds(x.plan, bound)) {
+            if (x.bound >= bound && plan_holds(x.plan, bound)) {
                 g = &x;
                 break;
             }

@@ -1156,9 +1156,11 @@ static void launch_wide(const void* A, int lda, const void* W, float wscale, int
 template <int BM, int BN, int WGM, int WGN, typename Epi>
 static void launch_f16(const void* A, int lda, const void* W, float wscale, int N, int K,
                        const int* m_dev, int m_cap, int splits, float* part, const Epi& epi,
-                       hipStream_t s, int pair_cus = 0) {
+                       hipStream_t s, int pair_cus = 0, int m_rows = 0) {
     if (m_cap <= 0) return;
-    const int tiles = ((m_cap + BM - 1) / BM) * (N / BN) * splits;
+    // sized for m_rows (the rows known on the host, at most m_cap) when given
+    const int m_size = m_rows > 0 ? std::min(m_rows, m_cap) : m_cap;
+    const int tiles = ((m_size + BM - 1) / BM) * (N / BN) * splits;
     // persistent grid: as many workgroups as the CUs hold at once
     auto grid_for = [&](const void* kern) {
         return std::min(((tiles + 7) / 8) * 8, std::max(8, (g_cus * resident(kern) / 8) * 8));
@@ -1202,20 +1204,29 @@ static thread_local std::vector<GemmPlan>* g_plan_log = nullptr;
 void gemm_row_bound(int rows) { g_row_bound = rows; }
 void gemm_plan_log(std::vector<GemmPlan>* log) { g_plan_log = log; }
 
+// rows known on the host, exactly (no device count) or as an upper bound
+// (0: neither)
+static int host_rows(bool m_dev, int m_cap, int row_bound) {
+    return !m_dev ? m_cap : row_bound >= 0 ? std::max(1, std::min(row_bound, m_cap)) : 0;
+}
+
 // the kernels of a product of N x K weights over up to m_cap rows (m_dev: the
 // row count is read on the device), under the calling thread's row bound
 static int plan_kernels(int N, int K, bool m_dev, int m_cap, int splits, bool wide_ok,
                         int row_bound) {
     const long t256 = (long)((m_cap + 255) / 256) * (N / 256) * splits;
-    const long t128 = (long)((m_cap + 127) / 128) * (N / 128) * splits;
     const bool fit = wide_ok && N % 256 == 0 && (K / splits) % kWideK == 0;
-    const int small = N % 128 == 0 && t128 >= 512 ? kGemm128 : kGemm64;
+    const int m_host = host_rows(m_dev, m_cap, row_bound);
+    // the smaller tiles: 128 x 128 once they fill the CUs twice over, else
+    // 64 x 64 (4 stages deep up to 512 tiles, as launch_f16 sizes them)
+    const int m_sel = m_host > 0 ? m_host : m_cap;
+    const long t128 = (long)((m_sel + 127) / 128) * (N / 128) * splits;
+    const long t64 = (long)((m_sel + 63) / 64) * (N / 64) * splits;
+    const int small = N % 128 == 0 && t128 >= 512 ? kGemm128 : t64 <= 512 ? kGemm64 | kGemmDeep : kGemm64;
     if (g_force_tile != 0)   // HBSJD_GEMM_TILE: one kernel for every launch (results are the same)
         return g_force_tile > 0 && fit ? kGemmWide : small;
     const bool wide = fit && t256 >= kWideMin;
-    // rows known on the host, exactly (no device count) or as an upper bound:
-    // the kernel wide_pick picks for that many rows, alone
-    const int m_host = !m_dev ? m_cap : row_bound >= 0 ? std::max(1, std::min(row_bound, m_cap)) : 0;
+    // with host rows, the kernel wide_pick picks for that many rows, alone
     if (m_host > 0) return wide && wide_pick(m_host, N, K, splits, g_cus, true) != 0 ? kGemmWide : small;
     return wide ? small | kGemmPair : small;
 }
@@ -1234,10 +1245,13 @@ static void dispatch_f16(const void* A, int lda, const void* W, float wscale, in
     const int pair = k & kGemmPair ? g_cus : 0;
     if (k & (kGemmWide | kGemmPair))
         launch_wide(A, lda, W, wscale, N, K, m_dev, m_cap, splits, pair, part, epi, s);
+    const int m_rows = host_rows(m_dev != nullptr, m_cap, g_row_bound);
     if ((k & 3) == kGemm128)
-        launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
+        launch_f16<128, 128, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair,
+                                   m_rows);
     else if ((k & 3) == kGemm64)
-        launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair);
+        launch_f16<64, 64, 2, 2>(A, lda, W, wscale, N, K, m_dev, m_cap, splits, part, epi, s, pair,
+                                 m_rows);
 }
 
 // ---------------------------------------------------------------- fp32

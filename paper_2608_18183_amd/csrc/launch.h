@@ -90,11 +90,12 @@ hipError_t gemm_setup();
 // small only costs speed.
 void gemm_row_bound(int rows);
 // The kernels of one product (kGemmWide alone, kGemm128 or kGemm64 alone, or
-// kGemmPair | the smaller-tile kernel), recorded with its shape by every
-// product with a device row count while a log is set (null: none). A captured
-// round is valid for another row bound while gemm_plan() gives every product
-// it recorded the same kernels under that bound.
-enum { kGemmWide = 4, kGemm128 = 1, kGemm64 = 2, kGemmPair = 8 };
+// kGemmPair | the smaller-tile kernel; kGemmDeep marks the 4-stage 64 x 64
+// variant), recorded with its shape by every product with a device row count
+// while a log is set (null: none). A round captured under one row bound
+// serves a smaller bound while gemm_plan() gives every product it recorded
+// the same kernels under that bound (its launches are sized for the larger).
+enum { kGemmWide = 4, kGemm128 = 1, kGemm64 = 2, kGemmPair = 8, kGemmDeep = 16 };
 struct GemmPlan {
     int N, K, m_cap, splits;
     bool wide_ok;
