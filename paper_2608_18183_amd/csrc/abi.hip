@@ -487,6 +487,14 @@ hbsjd_status validate_args(const hbsjd_ctx* c, const hbsjd_rollout_args* a) {
     return HBSJD_OK;
 }
 
+// The products of the calling thread take a row bound until the end of
+// scope: an upper bound of a round's rows, or the exact rows of a forward whose
+// row count the host set itself.
+struct RowBound {
+    explicit RowBound(int rows) { gemm_row_bound(rows); }
+    ~RowBound() { gemm_row_bound(-1); }
+};
+
 hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_dev) {
     if (!c->weights) return fail(HBSJD_ESTATE, "weights not loaded");
     TRY(validate_args(c, a));
@@ -655,6 +663,7 @@ hbsjd_status begin(hbsjd_ctx* c, const hbsjd_rollout_args* a, int32_t* counts_de
                Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0), as<int32_t>(c->seg_nrows),
                         as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
                mp + kMetaSegs, n_seq, maxlen};
+    RowBound rb(pf_rows);
     forward_layers(c, fr);
     if (ar) {   // the prefill only fills the cache
         HIPTRY(c, hipGetLastError());
@@ -691,11 +700,6 @@ int round_row_bound(const hbsjd_ctx* c) {
     return (full ? c->B : std::min(c->a_bound, c->B)) * c->cfg * (c->W + 1);
 }
 
-// the products of the calling thread take a row bound until the end of scope
-struct RowBound {
-    explicit RowBound(int rows) { gemm_row_bound(rows); }
-    ~RowBound() { gemm_row_bound(-1); }
-};
 
 // queue the launches of one round on buffer parity `cur`; every launch sizes
 // itself from the device counts the round's set-up kernel writes
@@ -928,6 +932,7 @@ hbsjd_status forward_core(hbsjd_ctx* c, int n_images, const int32_t* tokens,
                Segments{as<int32_t>(c->seg_seq), as<int32_t>(c->seg_row0),
                         as<int32_t>(c->seg_nrows), as<int32_t>(c->seg_pos0), as<int32_t>(c->seg_pages)},
                mp + kMetaSegs, n_seqs, maxlen};
+    RowBound rb(rows);
     forward_layers(c, fr);
     HIPTRY(c, hipGetLastError());
     return HBSJD_OK;
@@ -1290,6 +1295,7 @@ hbsjd_status hbsjd_forward(hbsjd_ctx* c, int32_t n_seqs, const int32_t* tokens,
         }
         TRY(forward_core(c, n_seqs, tokens, lab, ln, simg, ln, row0));
         const int rows = row0.back();
+        RowBound rb(rows);
         gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d,
                     as<int32_t>(c->meta_pf) + kMetaRows, rows, logits, c->b_lm, c->stream);
         HIPTRY(c, hipGetLastError());
@@ -1368,6 +1374,7 @@ hbsjd_status hbsjd_score_bikl(hbsjd_ctx* student, hbsjd_ctx* teacher, int32_t B,
                                          hipMemcpyHostToDevice, c->stream));
                 int32_t* mp = as<int32_t>(c->meta_pf);
                 HIPTRY(c, hipMemcpyAsync(mp + kMetaActive, &nsel, 4, hipMemcpyHostToDevice, c->stream));
+                RowBound rb(nsel);
                 rmsnorm(c->f16, as<float>(c->h), as<int32_t>(c->lm_idx), mp + kMetaActive, nsel,
                         c->g_out, c->m.rms_eps, c->d, c->hb.p, c->stream);
                 gemm_logits(c->f16, c->hb.p, c->d, c->w_lm, c->s_lm, c->V, c->d, mp + kMetaActive, nsel,
