@@ -99,6 +99,65 @@ __device__ __forceinline__ void stage_store_row(float* __restrict__ row, int V, 
     }
 }
 
+// One thread's sequential sums over LDS in the pinned order. The reads of
+// each group of 16 entries are issued before the adds of the previous group,
+// so the chain of adds does not wait on an LDS round trip every few entries.
+// seq_sum_lds returns ((v[0] + v[1]) + ...) + v[n-1] (0 + ... from zero);
+// seq_prefix_lds turns v[0..n-1] into its inclusive running sums from zero.
+constexpr int kSeqGroup = 16;
+__device__ inline float seq_sum_lds(const float* v, int n) {
+    float z = 0.f;
+    const int groups = n / kSeqGroup;
+    if (groups > 0) {
+        float cur[kSeqGroup];
+#pragma unroll
+        for (int k = 0; k < kSeqGroup; ++k) cur[k] = v[k];
+        for (int g = 1; g < groups; ++g) {
+            float nxt[kSeqGroup];
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) nxt[k] = v[kSeqGroup * g + k];
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) z = z + cur[k];
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) cur[k] = nxt[k];
+        }
+#pragma unroll
+        for (int k = 0; k < kSeqGroup; ++k) z = z + cur[k];
+    }
+    for (int i = kSeqGroup * groups; i < n; ++i) z = z + v[i];
+    return z;
+}
+__device__ inline void seq_prefix_lds(float* v, int n) {
+    float run = 0.f;
+    const int groups = n / kSeqGroup;
+    if (groups > 0) {
+        float cur[kSeqGroup];
+#pragma unroll
+        for (int k = 0; k < kSeqGroup; ++k) cur[k] = v[k];
+        for (int g = 1; g < groups; ++g) {
+            float nxt[kSeqGroup];
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) nxt[k] = v[kSeqGroup * g + k];
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) {
+                run = run + cur[k];
+                v[kSeqGroup * (g - 1) + k] = run;
+            }
+#pragma unroll
+            for (int k = 0; k < kSeqGroup; ++k) cur[k] = nxt[k];
+        }
+#pragma unroll
+        for (int k = 0; k < kSeqGroup; ++k) {
+            run = run + cur[k];
+            v[kSeqGroup * (groups - 1) + k] = run;
+        }
+    }
+    for (int i = kSeqGroup * groups; i < n; ++i) {
+        run = run + v[i];
+        v[i] = run;
+    }
+}
+
 // order-preserving map of a float to an int (and back), for exact LDS min/max
 __device__ inline int float_key(float f) {
     const int i = __builtin_bit_cast(int, f);
@@ -342,9 +401,7 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     if (t < nC) tot[t] = csum;
     __syncthreads();
     if (t == 0) {
-        float z = 0.f;
-        for (int c = 0; c < nC; ++c) z = z + tot[c];
-        s_flt[1] = z;
+        s_flt[1] = seq_sum_lds(tot, nC);
         s_int[2] = -1;   // the row's last positive entry, gathered below
     }
     __syncthreads();
@@ -369,12 +426,8 @@ __global__ __launch_bounds__(256) void k_transform(TransformArgs a) {
     }
     __syncthreads();
     if (t == 0) {
-        float run = 0.f;
         tot[0] = 0.f;
-        for (int c = 0; c < nC; ++c) {
-            run = run + tot[c + 1];
-            tot[c + 1] = run;
-        }
+        seq_prefix_lds(tot + 1, nC);
     }
     __syncthreads();
 
@@ -463,12 +516,8 @@ __device__ inline int block_inv_cdf_regs(const float (&w)[kChunk], int V, float 
     if (t < nC) cp[t + 1] = sum;
     __syncthreads();
     if (t == 0) {
-        float run = 0.f;
         cp[0] = 0.f;
-        for (int c = 0; c < nC; ++c) {
-            run = run + cp[c + 1];
-            cp[c + 1] = run;
-        }
+        seq_prefix_lds(cp + 1, nC);
     }
     __syncthreads();
     const float total = cp[nC];
