@@ -1216,12 +1216,15 @@ static int plan_kernels(int N, int K, bool m_dev, int m_cap, int splits, bool wi
     const long t256 = (long)((m_cap + 255) / 256) * (N / 256) * splits;
     const bool fit = wide_ok && N % 256 == 0 && (K / splits) % kWideK == 0;
     const int m_host = host_rows(m_dev, m_cap, row_bound);
-    // the smaller tiles: 128 x 128 once they fill the CUs twice over, else
-    // 64 x 64 (4 stages deep up to 512 tiles, as launch_f16 sizes them)
+    // the smaller tiles: 64 x 64 while the CUs hold all of them at once (3 per
+    // CU; 4 stages deep up to 512 tiles, as launch_f16 sizes them), else
+    // 128 x 128. Measured with the partial-sum store at 132-5478 rows of the
+    // XL products: once 64 x 64 needs a second round, 128 x 128 took at most
+    // as long (W2 at 2640 rows 51 -> 40 us), except QKV at 1188 rows (23 ->
+    // 26 us), where the wide kernel works.
     const int m_sel = m_host > 0 ? m_host : m_cap;
-    const long t128 = (long)((m_sel + 127) / 128) * (N / 128) * splits;
     const long t64 = (long)((m_sel + 63) / 64) * (N / 64) * splits;
-    const int small = N % 128 == 0 && t128 >= 512 ? kGemm128 : t64 <= 512 ? kGemm64 | kGemmDeep : kGemm64;
+    const int small = N % 128 == 0 && t64 > 3L * g_cus ? kGemm128 : t64 <= 512 ? kGemm64 | kGemmDeep : kGemm64;
     if (g_force_tile != 0)   // HBSJD_GEMM_TILE: one kernel for every launch (results are the same)
         return g_force_tile > 0 && fit ? kGemmWide : small;
     const bool wide = fit && t256 >= kWideMin;
