@@ -290,6 +290,30 @@ def test_rollout_bf16_full_equals_compact_and_counts_are_bounded():
     assert (t0 >= 0).all() and (t0 < shape.vocab).all()
 
 
+def test_rollout_bf16_full_equals_compact_across_kernel_choices():
+    """With 192 images of the B model a Full round has 3264 rows, enough for
+    the wide GEMM kernel on QKV, W1|W3 and the lm_head, while Compact rounds
+    size their kernels for the active images only (the host's row bound), so
+    the two modes run different kernels as images finish (prefix lengths
+    spread over the grid). Tokens and counts must still agree bit for bit,
+    with AUTO switching between the two at gamma = 96."""
+    wl = synth.WORKLOADS["llamagen_b"]
+    shape = wl.model
+    blob = synth.make_weights(shape, 0)
+    batch = synth.make_batch(wl, 7, batch=192)
+    batch.prefix_len[:] = np.linspace(0, shape.T - 2, 192).astype(batch.prefix_len.dtype)
+    ctx = gu.make_ctx(shape, "bf16", blob)
+    outs = [ctx.hbsjd_rollout(gu.device_batch(batch), batch.prefix_len, batch.labels,
+                              batch.temperature, wl.window, top_k=wl.top_k, seed=1003,
+                              exec_mode=mode, gamma=96)
+            for mode in (P().EXEC_FULL, P().EXEC_COMPACT, P().EXEC_AUTO)]
+    t0 = outs[0]["tokens"].cpu().numpy()
+    for o in outs[1:]:
+        assert np.array_equal(o["tokens"].cpu().numpy(), t0)
+        assert np.array_equal(o["counts"].cpu().numpy(), outs[0]["counts"].cpu().numpy())
+    assert outs[0]["rounds"] > 10
+
+
 @pytest.mark.parametrize("kernel", ["seq", "split"])
 def test_forward_bf16_each_attention_kernel_matches_oracle(kernel, monkeypatch):
     """Two of the attention kernels (causal attention of each sequence's rows
